@@ -1,0 +1,159 @@
+"""TEST INFRASTRUCTURE ONLY: the CPU oracle for batched tree verification.
+
+A plain, slow, obviously correct evaluation (``oracle.c``, fp64, OpenMP)
+of tree attention, per-node argmax and longest-accepted-path acceptance,
+written from the paper's definitions (section 2 draft token trees;
+section 3 Theorem 1 path acceptance; section 4.3 step 4 verification;
+section 5.1 logits returned per node; Appendix B parents before children).
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  It shares no code with the HIP
+library and never imports it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "_build", "liboracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile ``oracle.c`` with gcc into ``oracle/_build/liboracle.so``."""
+    if not force and os.path.exists(_LIB_PATH):
+        return _LIB_PATH
+    os.makedirs(os.path.dirname(_LIB_PATH), exist_ok=True)
+    tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-Wall", "-Wextra",
+           _SRC, "-o", tmp, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+    lib.oracle_tree_attn.restype = i32
+    lib.oracle_tree_attn.argtypes = [i32, P, P, P, P, i64, i32, P, P, P, P, P, i32,
+                                     i32, i32, i32, i32, f64, i32, P, P]
+    lib.oracle_node_argmax.restype = None
+    lib.oracle_node_argmax.argtypes = [P, i64, i32, i32, i32, P]
+    for name in ("oracle_tree_accept", "oracle_tree_accept_bruteforce"):
+        fn = getattr(lib, name)
+        fn.restype = None
+        fn.argtypes = [i32, P, P, P, P, i32, P, P, P]
+    lib.oracle_set_num_threads.restype = None
+    lib.oracle_set_num_threads.argtypes = [i32]
+    lib.oracle_get_num_threads.restype = i32
+    lib.oracle_get_num_threads.argtypes = []
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray) -> ctypes.c_void_p:
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def set_num_threads(n: int) -> None:
+    _load().oracle_set_num_threads(int(n))
+
+
+def num_threads() -> int:
+    return int(_load().oracle_get_num_threads())
+
+
+def tree_attn(*, node_indptr, parent, prefix_len, block_table, q, k_tree, v_tree,
+              k_pages, v_pages, dtype: str, num_q_heads: int, num_kv_heads: int,
+              head_dim: int, page_size: int, sm_scale: float,
+              nodes: Optional[Sequence[int]] = None) -> np.ndarray:
+    """Attention output (float64 ``[len(nodes), Hq, D]``) of the selected
+    global node ids (all nodes when ``nodes`` is None)."""
+    lib = _load()
+    indptr = _i32(node_indptr)
+    par = _i32(parent)
+    L = _i32(prefix_len)
+    bt = _i32(block_table)
+    if bt.ndim != 2:
+        raise ValueError("block_table must be 2-D")
+    T = int(indptr[-1])
+    sel = _i32(np.arange(T) if nodes is None else nodes)
+    is_bf16 = 1 if dtype == "bf16" else 0
+    want = np.uint16 if is_bf16 else np.float32
+    arrs = [np.ascontiguousarray(a, dtype=want) for a in (q, k_tree, v_tree, k_pages, v_pages)]
+    out = np.zeros((sel.size, num_q_heads, head_dim), dtype=np.float64)
+    rc = lib.oracle_tree_attn(int(indptr.size - 1), _ptr(indptr), _ptr(par), _ptr(L), _ptr(bt),
+                              int(bt.shape[1]), int(arrs[3].shape[0]),
+                              *[_ptr(a) for a in arrs], is_bf16,
+                              int(num_q_heads), int(num_kv_heads), int(head_dim), int(page_size),
+                              float(sm_scale), int(sel.size), _ptr(sel), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_tree_attn: malformed input")
+    return out
+
+
+def tree_attn_batch(batch, nodes: Optional[Sequence[int]] = None) -> np.ndarray:
+    """``tree_attn`` on a ``VerifyBatch``."""
+    return tree_attn(node_indptr=batch.node_indptr, parent=batch.parent,
+                     prefix_len=batch.prefix_len, block_table=batch.block_table,
+                     q=batch.q, k_tree=batch.k_tree, v_tree=batch.v_tree,
+                     k_pages=batch.k_pages, v_pages=batch.v_pages, dtype=batch.dtype,
+                     num_q_heads=batch.num_q_heads, num_kv_heads=batch.num_kv_heads,
+                     head_dim=batch.head_dim, page_size=batch.page_size,
+                     sm_scale=batch.sm_scale, nodes=nodes)
+
+
+def node_argmax(logits: np.ndarray, vocab: int, dtype: str,
+                rows: Optional[Sequence[int]] = None) -> np.ndarray:
+    """First-maximum argmax of each logits row (or of the selected rows)."""
+    lib = _load()
+    want = np.uint16 if dtype == "bf16" else np.float32
+    lg = np.ascontiguousarray(logits, dtype=want)
+    if rows is not None:
+        lg = np.ascontiguousarray(lg[np.asarray(rows, dtype=np.int64)])
+    out = np.empty(lg.shape[0], dtype=np.int32)
+    lib.oracle_node_argmax(_ptr(lg), int(lg.shape[1]), int(lg.shape[0]), int(vocab),
+                           1 if dtype == "bf16" else 0, _ptr(out))
+    return out
+
+
+def _accept(fn_name, node_indptr, parent, draft_tokens, target_argmax, max_accept):
+    lib = _load()
+    indptr, par = _i32(node_indptr), _i32(parent)
+    draft, amax = _i32(draft_tokens), _i32(target_argmax)
+    B = int(indptr.size - 1)
+    alen = np.empty(B, dtype=np.int32)
+    tok = np.empty((B, max_accept), dtype=np.int32)
+    nodes = np.empty((B, max_accept), dtype=np.int32)
+    getattr(lib, fn_name)(B, _ptr(indptr), _ptr(par), _ptr(draft), _ptr(amax), int(max_accept),
+                          _ptr(alen), _ptr(tok), _ptr(nodes))
+    return alen, tok, nodes
+
+
+def tree_accept(node_indptr, parent, draft_tokens, target_argmax, max_accept: int):
+    """Topological acceptance: returns ``(accept_len, accept_tokens, accept_nodes)``."""
+    return _accept("oracle_tree_accept", node_indptr, parent, draft_tokens, target_argmax,
+                   max_accept)
+
+
+def tree_accept_bruteforce(node_indptr, parent, draft_tokens, target_argmax, max_accept: int):
+    """Acceptance by enumerating every root-to-leaf path (same outputs)."""
+    return _accept("oracle_tree_accept_bruteforce", node_indptr, parent, draft_tokens,
+                   target_argmax, max_accept)
