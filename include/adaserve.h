@@ -1,0 +1,168 @@
+/*
+ * adaserve.h -- C ABI of the MI355X (gfx950) batched tree-verification library.
+ *
+ * One verification pass of SLO-customised speculative decoding (section 4.3,
+ * step 4): the target model scores every node of every request's draft token
+ * tree in one pass, and the tokens to commit are read off the logits of those
+ * nodes (section 5.1).  The library provides the three steps of that pass
+ * that run after the projections:
+ *
+ *   adaserve_tree_attn_verify  paged tree attention: each node attends to its
+ *                              request's cached prefix plus its own
+ *                              root-to-node path (section 2, draft token tree;
+ *                              section 3, Theorem 1's root-to-v paths);
+ *   adaserve_node_argmax       the target's greedy choice at every node;
+ *   adaserve_tree_accept       the longest accepted root path per request and
+ *                              the tokens it commits.
+ *
+ * Conventions for every entry point:
+ *  - Pointers without a _host suffix are DEVICE pointers owned by the caller;
+ *    _host pointers are host memory read synchronously during the call and
+ *    not retained.  Nothing is allocated or freed, and nothing synchronises:
+ *    work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
+ *    the call returns.
+ *  - Every scalar, pointer and host-mirror value is validated on the host
+ *    before anything is enqueued; on a non-OK status nothing was enqueued and
+ *    adaserve_last_error() describes the problem.
+ *  - Device-only contents (parent arrays, block tables, draft tokens) are
+ *    checked in the kernels: malformed trees give accept_len = -1 in
+ *    adaserve_tree_accept and unspecified (but in-bounds) attention output.
+ *  - The library is stateless apart from a per-device architecture check and
+ *    the thread-local error string; calls on different streams may overlap.
+ *  - Only gfx950 devices are supported (ADASERVE_ERR_UNSUPPORTED otherwise).
+ *
+ * Tree encoding (all entry points): request r owns the global node rows
+ * [node_indptr[r], node_indptr[r+1]); local node 0 is the root (the last
+ * committed token); parent[] holds LOCAL parent ids with parent[root] = -1 and
+ * 0 <= parent[i] < i for every other node (a parent is drafted before its
+ * children, Appendix B).  1 <= N_r <= 128 nodes per request.
+ */
+#ifndef ADASERVE_H
+#define ADASERVE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes returned by every entry point. */
+#define ADASERVE_OK                   0
+#define ADASERVE_ERR_INVALID_ARGUMENT 1  /* bad pointer, size, layout or host-mirror value   */
+#define ADASERVE_ERR_UNSUPPORTED      2  /* valid but not built: head_dim, page size, device  */
+#define ADASERVE_ERR_WORKSPACE        3  /* workspace missing or smaller than required        */
+#define ADASERVE_ERR_DEVICE           4  /* a HIP runtime call or kernel launch failed        */
+
+/* Element types of the floating-point tensors. */
+#define ADASERVE_F32  0
+#define ADASERVE_BF16 1
+
+/* Maximum tree nodes per request. */
+#define ADASERVE_MAX_TREE_NODES 128
+
+/*
+ * Bytes of device workspace adaserve_tree_attn_verify needs for this batch
+ * (split-KV partial results).  Depends only on the arguments given here, so a
+ * caller can size the workspace once per batch shape.  Returns 0 when no
+ * workspace is needed and SIZE_MAX when the arguments are invalid (the
+ * reason is in adaserve_last_error()).
+ */
+size_t adaserve_tree_attn_workspace_bytes(int32_t num_requests, const int32_t *node_indptr_host,
+                                          const int32_t *prefix_len_host, int32_t num_q_heads,
+                                          int32_t num_kv_heads, int32_t head_dim,
+                                          int32_t page_size, int32_t dtype);
+
+/*
+ * Paged tree attention (section 4.3 step 4; section 2 draft token tree).
+ *
+ * For node i of request r and q-head h, with kv-head g = h / (Hq / Hkv)
+ * (contiguous head groups), the output is softmax-weighted attention of
+ * q[i, h] over, in this order,
+ *   - the request's cached prefix: positions t = 0 .. L_r - 1, held in page
+ *     block_table[r * block_table_stride + t / page_size], slot t % page_size;
+ *   - the tree nodes on i's root-to-node path (root .. i, i included), whose
+ *     keys and values are k_tree / v_tree rows of those nodes;
+ * with scores sm_scale * <q, k>.  No other tree node is visible to i.  The
+ * kernel applies no positional encoding: q and k_tree arrive post-RoPE.
+ *
+ * Layouts (row-major, dense):
+ *   q, out            [T, Hq, D]              dtype
+ *   k_tree, v_tree    [T, Hkv, D]             dtype
+ *   k_pages, v_pages  [num_pages, Hkv, page_size, D]   dtype
+ *   block_table       [num_requests, block_table_stride] int32 physical page ids
+ *   prefix_len        [num_requests] int32 (device), prefix_len_host its host copy
+ *   node_indptr       [num_requests + 1] int32 (device), node_indptr_host its copy
+ * Supported: dtype F32 or BF16; head_dim 64 or 128; page_size 16; any
+ * Hq % Hkv == 0 with Hq / Hkv <= 16; L_r >= 0 (L_r = 0: attention over the
+ * root path only).  BF16 computes Q.K^T and P.V on bf16 matrix cores with
+ * fp32 accumulation and rounds the output to bf16 (nearest even); F32 computes
+ * in fp32 throughout.
+ * Slots past L_r in the last page and pages not listed for r are never read
+ * into the result (they may hold NaN).  Block-table entries outside
+ * [0, num_pages) are treated as all-zero pages.  The device arrays must equal
+ * their host mirrors.  workspace must hold at least
+ * adaserve_tree_attn_workspace_bytes(...) bytes (256-byte aligned).
+ */
+int32_t adaserve_tree_attn_verify(int32_t num_requests, const int32_t *node_indptr,
+                                  const int32_t *node_indptr_host, const int32_t *parent,
+                                  const void *q, const void *k_tree, const void *v_tree,
+                                  const void *k_pages, const void *v_pages, int32_t num_pages,
+                                  const int32_t *block_table, int32_t block_table_stride,
+                                  const int32_t *prefix_len, const int32_t *prefix_len_host,
+                                  int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                  int32_t page_size, float sm_scale, int32_t dtype, void *out,
+                                  void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Per-node vocabulary argmax of the verification logits (section 5.1: the
+ * logits of every node come back from verification and the verified tokens
+ * are identified from them; greedy reading: the target's choice is its
+ * highest-scoring token).
+ *
+ * logits: [num_rows, row_stride] of dtype, row i = logits + i * row_stride
+ * elements, columns 0 .. vocab - 1 compared (the rest of a row is never read).
+ * argmax_out: [num_rows] int32, the LOWEST index holding the row's maximum
+ * (values compare after exact widening to fp32; +0 == -0).  NaN inputs give
+ * an unspecified index in [0, vocab).  Requires vocab >= 1 when num_rows > 0,
+ * row_stride >= vocab.  num_rows = 0 is a no-op.
+ */
+int32_t adaserve_node_argmax(const void *logits, int64_t row_stride, int32_t num_rows,
+                             int32_t vocab, int32_t dtype, int32_t *argmax_out, void *stream);
+
+/*
+ * Longest-accepted-path acceptance (greedy tree verification, section 4.3
+ * step 4, read with section 2's tree and Algorithm 2's count of the root as
+ * one accepted token).
+ *
+ * Node j > 0 matches when draft_tokens[j] == target_argmax[parent(j)]; j is
+ * accepted when every non-root node on its root-to-node path matches; the
+ * root is always accepted and its draft token is never compared.  With d* the
+ * largest depth of an accepted node (root depth 0) and i* the smallest local
+ * id among accepted nodes of that depth:
+ *   accept_len[r]              = d* + 1
+ *   accept_nodes[r][k]         = local id of the depth-k node on the root..i*
+ *                                path, k = 0..d*
+ *   accept_tokens[r][k]        = draft token of accept_nodes[r][k + 1], k < d*
+ *   accept_tokens[r][d*]       = target_argmax[i*]  (the target's next token)
+ *   slots k > d*               = -1
+ * Outputs are [num_requests, max_accept] int32 rows (row stride max_accept).
+ * A request whose tree is malformed (N_r outside 1..128, indptr outside
+ * [0, total_nodes], parent[root] != -1, a parent not earlier than its child)
+ * or deeper than max_accept - 1 gets accept_len = -1 and -1 in every slot.
+ * draft_tokens, target_argmax: [total_nodes] int32 (device).
+ */
+int32_t adaserve_tree_accept(int32_t num_requests, int32_t total_nodes,
+                             const int32_t *node_indptr, const int32_t *parent,
+                             const int32_t *draft_tokens, const int32_t *target_argmax,
+                             int32_t max_accept, int32_t *accept_len, int32_t *accept_tokens,
+                             int32_t *accept_nodes, void *stream);
+
+/* Message describing the last non-OK status returned on this thread. */
+const char *adaserve_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ADASERVE_H */

@@ -1,0 +1,273 @@
+// Host side of the C ABI declared in include/adaserve.h: argument
+// validation (pure host code, runs before any HIP call), the split-KV work
+// planner, the gfx950 device check and the kernel launches.
+#include "adaserve.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+
+#include "kernels.h"
+#include "plan.h"
+
+namespace {
+
+using namespace adaserve;
+
+thread_local std::string g_last_error;
+
+int32_t fail(int32_t code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// gfx950 check, once per device ordinal.
+int32_t check_device() {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(ADASERVE_ERR_DEVICE, "hipGetDevice failed: %s", hipGetErrorString(e));
+  static std::mutex mu;
+  static signed char verdict[256];  // 0 unknown, 1 gfx950, -1 other
+  if (dev < 0 || dev >= 256) return fail(ADASERVE_ERR_DEVICE, "device ordinal %d out of range", dev);
+  std::lock_guard<std::mutex> lock(mu);
+  if (verdict[dev] == 0) {
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess)
+      return fail(ADASERVE_ERR_DEVICE, "hipGetDeviceProperties failed: %s", hipGetErrorString(e));
+    verdict[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
+    if (verdict[dev] < 0) g_last_error = std::string("unsupported device architecture ") + prop.gcnArchName;
+  }
+  if (verdict[dev] < 0) return fail(ADASERVE_ERR_UNSUPPORTED, "device %d is not gfx950", dev);
+  return ADASERVE_OK;
+}
+
+int32_t launch_status(hipError_t e, const char *what) {
+  if (e == hipSuccess) return ADASERVE_OK;
+  return fail(ADASERVE_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+struct AttnShape {
+  int32_t num_requests = 0;
+  int32_t total_nodes = 0;
+  int32_t group = 0;
+};
+
+// Scalar and host-mirror validation shared by the workspace query and the
+// verify call.  Does not touch device memory.
+int32_t validate_attn_shape(int32_t num_requests, const int32_t *indptr_host, const int32_t *plen_host,
+                            int32_t hq, int32_t hkv, int32_t head_dim, int32_t page_size, int32_t dtype,
+                            int32_t bt_stride_or_neg, AttnShape &shape) {
+  if (num_requests < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_requests %d < 0", num_requests);
+  if (hq <= 0 || hkv <= 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "head counts must be positive (%d, %d)", hq, hkv);
+  if (hq % hkv != 0)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_q_heads %d is not a multiple of num_kv_heads %d", hq, hkv);
+  if (hq / hkv > 16) return fail(ADASERVE_ERR_UNSUPPORTED, "head group %d > 16", hq / hkv);
+  if (dtype != ADASERVE_F32 && dtype != ADASERVE_BF16) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
+  if (head_dim != 64 && head_dim != 128) return fail(ADASERVE_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
+  if (page_size != kPageSize) return fail(ADASERVE_ERR_UNSUPPORTED, "page_size %d (supported: 16)", page_size);
+  shape.num_requests = num_requests;
+  shape.group = hq / hkv;
+  if (num_requests == 0) return ADASERVE_OK;
+  if (!indptr_host || !plen_host) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "host mirrors must not be NULL");
+  if (indptr_host[0] != 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "node_indptr[0] = %d, expected 0", indptr_host[0]);
+  int64_t total = 0;
+  for (int32_t r = 0; r < num_requests; ++r) {
+    const int64_t n = (int64_t)indptr_host[r + 1] - indptr_host[r];
+    if (n < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "request %d has %lld tree nodes (need >= 1)", r, (long long)n);
+    if (n > kMaxTreeNodes) return fail(ADASERVE_ERR_UNSUPPORTED, "request %d has %lld tree nodes (max %d)", r, (long long)n, kMaxTreeNodes);
+    total += n;
+    const int32_t L = plen_host[r];
+    if (L < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "prefix_len[%d] = %d < 0", r, L);
+    if (bt_stride_or_neg >= 0 && ceil_div(L, kPageSize) > bt_stride_or_neg)
+      return fail(ADASERVE_ERR_INVALID_ARGUMENT, "prefix_len[%d] = %d needs %d pages > block_table_stride %d", r, L,
+                  ceil_div(L, kPageSize), bt_stride_or_neg);
+  }
+  if (total > INT32_MAX / 16) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "too many tree nodes (%lld)", (long long)total);
+  shape.total_nodes = (int32_t)total;
+  return ADASERVE_OK;
+}
+
+struct AttnPlan {
+  int32_t chunk_keys = 0;
+  int64_t units = 0;
+  int64_t padded_grid = 0;
+  int64_t row_groups = 0;
+  bool needs_combine = false;
+  size_t ws_o_bytes = 0;
+  size_t ws_bytes = 0;
+};
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Split-KV plan.  Chooses the prefix chunk (a power of two between 256 and
+// 8192 keys) so that the batch has about 1024 work units: enough to keep
+// 256 CUs busy with two resident workgroups each while leaving partials
+// rare.  Depends only on host-visible sizes.
+AttnPlan make_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
+                   int32_t group, int32_t head_dim, int32_t dtype) {
+  AttnPlan p;
+  if (dtype != ADASERVE_BF16 || B == 0) return p;
+  int64_t work = 0;
+  for (int32_t r = 0; r < B; ++r) {
+    const int32_t n = indptr_host[r + 1] - indptr_host[r];
+    work += (int64_t)hkv * row_tiles(n, group) * (int64_t)(plen_host[r] > 0 ? plen_host[r] : 1);
+  }
+  const int64_t target_units = 1024;
+  int32_t chunk = 256;
+  while (chunk < 8192 && (int64_t)chunk * target_units < work) chunk *= 2;
+  p.chunk_keys = chunk;
+  for (int32_t r = 0; r < B; ++r) {
+    const int32_t n = indptr_host[r + 1] - indptr_host[r];
+    const int32_t c = prefix_chunks(plen_host[r], chunk);
+    p.units += request_units(n, plen_host[r], hkv, group, chunk);
+    p.row_groups += (int64_t)hkv * row_tiles(n, group);
+    if (c > 1) p.needs_combine = true;
+  }
+  p.padded_grid = pad_to_xcds(p.units);
+  if (p.needs_combine) {
+    p.ws_o_bytes = round_up((size_t)p.units * kRowsPerTile * head_dim * sizeof(float), 256);
+    p.ws_bytes = p.ws_o_bytes + round_up((size_t)p.units * kRowsPerTile * 2 * sizeof(float), 256);
+  }
+  return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *adaserve_last_error(void) { return g_last_error.c_str(); }
+
+size_t adaserve_tree_attn_workspace_bytes(int32_t num_requests, const int32_t *node_indptr_host,
+                                          const int32_t *prefix_len_host, int32_t num_q_heads,
+                                          int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
+                                          int32_t dtype) {
+  AttnShape shape;
+  if (validate_attn_shape(num_requests, node_indptr_host, prefix_len_host, num_q_heads, num_kv_heads,
+                          head_dim, page_size, dtype, -1, shape) != ADASERVE_OK)
+    return SIZE_MAX;
+  return make_plan(num_requests, node_indptr_host, prefix_len_host, num_kv_heads, shape.group, head_dim, dtype)
+      .ws_bytes;
+}
+
+int32_t adaserve_tree_attn_verify(int32_t num_requests, const int32_t *node_indptr,
+                                  const int32_t *node_indptr_host, const int32_t *parent, const void *q,
+                                  const void *k_tree, const void *v_tree, const void *k_pages,
+                                  const void *v_pages, int32_t num_pages, const int32_t *block_table,
+                                  int32_t block_table_stride, const int32_t *prefix_len,
+                                  const int32_t *prefix_len_host, int32_t num_q_heads, int32_t num_kv_heads,
+                                  int32_t head_dim, int32_t page_size, float sm_scale, int32_t dtype,
+                                  void *out, void *workspace, size_t workspace_bytes, void *stream) {
+  if (block_table_stride < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "block_table_stride < 0");
+  if (num_pages < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_pages < 0");
+  if (!std::isfinite(sm_scale)) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "sm_scale is not finite");
+  AttnShape shape;
+  int32_t st = validate_attn_shape(num_requests, node_indptr_host, prefix_len_host, num_q_heads, num_kv_heads,
+                                   head_dim, page_size, dtype, block_table_stride, shape);
+  if (st != ADASERVE_OK) return st;
+  if (num_requests == 0) return ADASERVE_OK;
+  if (!node_indptr || !parent || !q || !k_tree || !v_tree || !out || !prefix_len)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  bool any_prefix = false;
+  for (int32_t r = 0; r < num_requests; ++r) any_prefix |= prefix_len_host[r] > 0;
+  if (any_prefix) {
+    if (!k_pages || !v_pages || !block_table)
+      return fail(ADASERVE_ERR_INVALID_ARGUMENT, "k_pages, v_pages and block_table are required when a prefix is non-empty");
+    if (num_pages < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_pages must be >= 1 when a prefix is non-empty");
+  }
+  const void *tensors[] = {q, k_tree, v_tree, out, k_pages, v_pages};
+  for (const void *t : tensors)
+    if (t && !aligned(t, 16)) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "tensor pointers must be 16-byte aligned");
+  const AttnPlan plan =
+      make_plan(num_requests, node_indptr_host, prefix_len_host, num_kv_heads, shape.group, head_dim, dtype);
+  if (plan.ws_bytes > 0) {
+    if (!workspace || workspace_bytes < plan.ws_bytes)
+      return fail(ADASERVE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.ws_bytes,
+                  workspace ? workspace_bytes : (size_t)0);
+    if (!aligned(workspace, 256)) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  }
+  st = check_device();
+  if (st != ADASERVE_OK) return st;
+
+  TreeAttnArgs a{};
+  a.node_indptr = node_indptr;
+  a.parent = parent;
+  a.prefix_len = prefix_len;
+  a.block_table = block_table;
+  a.bt_stride = block_table_stride;
+  a.num_pages = num_pages;
+  a.q = q;
+  a.k_tree = k_tree;
+  a.v_tree = v_tree;
+  a.k_pages = k_pages;
+  a.v_pages = v_pages;
+  a.out = out;
+  a.ws_o = plan.ws_bytes ? (float *)workspace : nullptr;
+  a.ws_ml = plan.ws_bytes ? (float *)((char *)workspace + plan.ws_o_bytes) : nullptr;
+  a.num_requests = num_requests;
+  a.total_nodes = shape.total_nodes;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.group = shape.group;
+  a.chunk_keys = plan.chunk_keys;
+  a.units = plan.units;
+  a.padded_grid = plan.padded_grid;
+  a.row_groups = plan.row_groups;
+  a.sm_scale = sm_scale;
+  a.scale_log2 = sm_scale * 1.4426950408889634f;
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == ADASERVE_BF16)
+    return launch_status(launch_tree_attn_bf16(a, head_dim, plan.needs_combine, s), "tree attention launch");
+  return launch_status(launch_tree_attn_f32(a, head_dim, s), "tree attention launch");
+}
+
+int32_t adaserve_node_argmax(const void *logits, int64_t row_stride, int32_t num_rows, int32_t vocab, int32_t dtype,
+                             int32_t *argmax_out, void *stream) {
+  if (num_rows < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_rows %d < 0", num_rows);
+  if (dtype != ADASERVE_F32 && dtype != ADASERVE_BF16) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
+  if (num_rows == 0) return ADASERVE_OK;
+  if (vocab < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "vocab %d < 1", vocab);
+  if (row_stride < vocab) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "row_stride %lld < vocab %d", (long long)row_stride, vocab);
+  if (!logits || !argmax_out) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "NULL logits or output");
+  const size_t esz = dtype == ADASERVE_BF16 ? 2 : 4;
+  if (!aligned(logits, esz) || !aligned(argmax_out, 4))
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "misaligned logits or output pointer");
+  const int32_t st = check_device();
+  if (st != ADASERVE_OK) return st;
+  return launch_status(launch_node_argmax(logits, row_stride, num_rows, vocab, dtype == ADASERVE_BF16, argmax_out,
+                                          (hipStream_t)stream),
+                       "argmax launch");
+}
+
+int32_t adaserve_tree_accept(int32_t num_requests, int32_t total_nodes, const int32_t *node_indptr,
+                             const int32_t *parent, const int32_t *draft_tokens, const int32_t *target_argmax,
+                             int32_t max_accept, int32_t *accept_len, int32_t *accept_tokens, int32_t *accept_nodes,
+                             void *stream) {
+  if (num_requests < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_requests %d < 0", num_requests);
+  if (total_nodes < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "total_nodes %d < 0", total_nodes);
+  if (max_accept < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "max_accept %d < 1", max_accept);
+  if (num_requests == 0) return ADASERVE_OK;
+  if (!node_indptr || !accept_len || !accept_tokens || !accept_nodes)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  if (total_nodes > 0 && (!parent || !draft_tokens || !target_argmax))
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  const int32_t st = check_device();
+  if (st != ADASERVE_OK) return st;
+  return launch_status(launch_tree_accept(num_requests, total_nodes, node_indptr, parent, draft_tokens, target_argmax,
+                                          max_accept, accept_len, accept_tokens, accept_nodes, (hipStream_t)stream),
+                       "accept launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,134 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/adaserve.h declares, and rejects bad arguments on the host before
+any HIP call (so nothing here touches a device)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2501_12162_amd as ada
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "adaserve.h")
+FAKE = 0x1000   # never dereferenced: every call below fails validation first
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ada.library_path()):
+        from paper_2501_12162_amd.build import build
+        build()
+    return ada.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(adaserve_\w+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(ada.SIGNATURES)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def _ws(ip, pl, hq=32, hkv=8, d=128, ps=16, dtype=ada.ADASERVE_BF16):
+    ip = np.asarray(ip, np.int32)
+    pl = np.asarray(pl, np.int32)
+    return ada.load_library().adaserve_tree_attn_workspace_bytes(
+        int(pl.size), ip.ctypes.data, pl.ctypes.data, hq, hkv, d, ps, dtype)
+
+
+SIZE_MAX = ctypes.c_size_t(-1).value
+
+
+def test_workspace_query(lib):
+    assert _ws([0, 10], [100]) == 0                       # short prefix: no split
+    assert _ws([0, 32], [32768]) > 0                      # long prefix is split
+    assert _ws([0, 32], [32768], dtype=ada.ADASERVE_F32) == 0
+    assert _ws([0, 10], [100], hq=30, hkv=8) == SIZE_MAX
+    assert _ws([0, 10], [100], d=96) == SIZE_MAX
+    assert _ws([0, 10], [100], ps=32) == SIZE_MAX
+    assert _ws([0, 129], [100]) == SIZE_MAX
+    assert _ws([0, 0], [100]) == SIZE_MAX
+    assert _ws([1, 5], [100]) == SIZE_MAX
+    assert _ws([0, 5], [-1]) == SIZE_MAX
+    assert b"prefix_len" in lib.adaserve_last_error()
+    assert _ws([], []) == 0
+
+
+def _verify(lib, **kw):
+    ip = np.asarray(kw.pop("ip", [0, 4]), np.int32)
+    pl = np.asarray(kw.pop("pl", [20]), np.int32)
+    args = dict(node_indptr=FAKE, parent=FAKE, q=FAKE, k_tree=FAKE, v_tree=FAKE, k_pages=FAKE,
+                v_pages=FAKE, num_pages=4, block_table=FAKE, bt_stride=2, prefix_len=FAKE,
+                hq=8, hkv=2, d=128, ps=16, scale=0.1, dtype=ada.ADASERVE_BF16, out=FAKE,
+                ws=None, ws_bytes=0)
+    args.update(kw)
+    return lib.adaserve_tree_attn_verify(
+        int(pl.size), args["node_indptr"], ip.ctypes.data, args["parent"], args["q"], args["k_tree"],
+        args["v_tree"], args["k_pages"], args["v_pages"], args["num_pages"], args["block_table"],
+        args["bt_stride"], args["prefix_len"], pl.ctypes.data, args["hq"], args["hkv"], args["d"],
+        args["ps"], args["scale"], args["dtype"], args["out"], args["ws"], args["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(hq=6, hkv=4), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(hq=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(hq=64, hkv=2), ada.ADASERVE_ERR_UNSUPPORTED),
+    (dict(d=80), ada.ADASERVE_ERR_UNSUPPORTED),
+    (dict(ps=8), ada.ADASERVE_ERR_UNSUPPORTED),
+    (dict(dtype=7), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(ip=[0, 200]), ada.ADASERVE_ERR_UNSUPPORTED),
+    (dict(ip=[0, 0]), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(ip=[2, 6]), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(pl=[-3]), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(pl=[33], bt_stride=2), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(bt_stride=-1), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(num_pages=-1), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(num_pages=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(scale=float("nan")), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(q=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(out=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(parent=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(k_pages=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(block_table=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(q=FAKE + 2), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(ip=[0, 32], pl=[32768], bt_stride=2048), ada.ADASERVE_ERR_WORKSPACE),
+])
+def test_verify_rejects_bad_arguments(lib, kw, code):
+    assert _verify(lib, **kw) == code
+    assert lib.adaserve_last_error()
+
+
+def test_verify_empty_batch_is_a_noop(lib):
+    assert _verify(lib, ip=[0], pl=[]) == ada.ADASERVE_OK
+
+
+def test_argmax_rejects_bad_arguments(lib):
+    f = lib.adaserve_node_argmax
+    assert f(FAKE, 10, -1, 10, 1, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+    assert f(FAKE, 10, 0, 10, 1, FAKE, None) == ada.ADASERVE_OK          # nothing to do
+    assert f(FAKE, 10, 3, 0, 1, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+    assert f(FAKE, 9, 3, 10, 1, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+    assert f(None, 10, 3, 10, 1, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+    assert f(FAKE, 10, 3, 10, 1, None, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+    assert f(FAKE, 10, 3, 10, 5, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+    assert f(FAKE + 1, 10, 3, 10, 1, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+
+
+def test_accept_rejects_bad_arguments(lib):
+    f = lib.adaserve_tree_accept
+    assert f(-1, 4, FAKE, FAKE, FAKE, FAKE, 4, FAKE, FAKE, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+    assert f(1, -4, FAKE, FAKE, FAKE, FAKE, 4, FAKE, FAKE, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+    assert f(1, 4, FAKE, FAKE, FAKE, FAKE, 0, FAKE, FAKE, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+    assert f(1, 4, None, FAKE, FAKE, FAKE, 4, FAKE, FAKE, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+    assert f(1, 4, FAKE, None, FAKE, FAKE, 4, FAKE, FAKE, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+    assert f(1, 4, FAKE, FAKE, FAKE, FAKE, 4, None, FAKE, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+    assert f(0, 0, None, None, None, None, 4, None, None, None, None) == ada.ADASERVE_OK

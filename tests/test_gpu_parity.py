@@ -1,0 +1,225 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bars (attention against the fp64 oracle):
+  * fp32: max |err| <= 1e-4;
+  * bf16: max |err| <= 2e-2 AND max |err| / max |ref| <= 1e-2 (the absolute
+    bar alone is loose for near-uniform softmaxes, whose outputs are small);
+  * every output finite although unused page slots and pages hold NaN;
+  * a mask-discriminating case where the masked and unmasked answers differ
+    by far more than the tolerance.
+Argmax indices, accept lengths, tokens and nodes: bit-exact.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from conftest import cached_config
+from paper_2501_12162_amd.workload import (bf16_bits_to_f32, chain_tree, f32_to_bf16_bits,
+                                            make_batch, make_tie_logits, random_tree)
+
+pytestmark = pytest.mark.gpu
+
+BF16_ABS, BF16_REL, F32_ABS = 2e-2, 1e-2, 1e-4
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2501_12162_amd as ada
+    ada.load_library()
+    return torch
+
+
+def run_device(b, max_accept=128):
+    from paper_2501_12162_amd.device import DeviceBatch
+    d = DeviceBatch(b, max_accept=max_accept)
+    d.step()
+    return d, d.results()
+
+
+def check_attention(b, out, nodes=None):
+    assert np.isfinite(out).all(), "non-finite attention output"
+    ref = oracle.tree_attn_batch(b, nodes=nodes)
+    got = out if nodes is None else out[np.asarray(nodes)]
+    err = float(np.abs(got - ref).max())
+    scale = float(np.abs(ref).max())
+    if b.dtype == "f32":
+        assert err <= F32_ABS, err
+    else:
+        assert err <= BF16_ABS, err
+        assert err <= BF16_REL * scale, (err, scale)
+    return err
+
+
+def check_argmax_accept(b, amax, alen, tok, nodes, max_accept=128):
+    ref_amax = oracle.node_argmax(b.logits, b.vocab, b.dtype)
+    np.testing.assert_array_equal(amax, ref_amax)
+    np.testing.assert_array_equal(amax, b.planted_argmax)
+    ra, rt, rn = oracle.tree_accept(b.node_indptr, b.parent, b.draft_tokens, ref_amax, max_accept)
+    np.testing.assert_array_equal(alen, ra)
+    np.testing.assert_array_equal(tok, rt)
+    np.testing.assert_array_equal(nodes, rn)
+
+
+def sample_nodes(b):
+    ip = b.node_indptr
+    s = set()
+    for r in range(b.num_requests):
+        a, e = int(ip[r]), int(ip[r + 1])
+        s.update({a, e - 1, (a + e) // 2})
+    return sorted(s)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_named_workload(torch_cuda, cfg):
+    b = cached_config(cfg)
+    print("workload", cfg, b.name, "T", b.total_nodes, flush=True)
+    _, (out, amax, alen, tok, nodes) = run_device(b)
+    check_attention(b, out, None if cfg == 1 else sample_nodes(b))
+    check_argmax_accept(b, amax, alen, tok, nodes)
+
+
+def _ragged_batch(dtype, head_dim, seed, hq=8, hkv=2):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    sizes = [1, 5, 33, 64, 100, 128]
+    lens = [0, 15, 64, 333, 1500, 5000]
+    parents = [chain_tree(1), random_tree(rng, 5), random_tree(rng, 33, 6), chain_tree(64),
+               random_tree(rng, 100, 10), random_tree(rng, 128)]
+    assert [len(p) for p in parents] == sizes
+    return make_batch(parents=parents, prefix_lens=lens, num_q_heads=hq, num_kv_heads=hkv,
+                      head_dim=head_dim, dtype=dtype, vocab=5003, seed=seed, row_pad=5)
+
+
+@pytest.mark.parametrize("dtype,head_dim,hq,hkv", [("bf16", 128, 8, 2), ("bf16", 64, 16, 2),
+                                                   ("bf16", 128, 16, 16), ("f32", 128, 4, 2),
+                                                   ("f32", 64, 8, 8)])
+def test_ragged_tiles_chunks_and_tails(torch_cuda, dtype, head_dim, hq, hkv):
+    b = _ragged_batch(dtype, head_dim, seed=31 + head_dim + hq, hq=hq, hkv=hkv)
+    d, (out, amax, alen, tok, nodes) = run_device(b)
+    if dtype == "bf16":
+        assert d.workspace_bytes > 0          # the long prefixes were split
+    check_attention(b, out)
+    check_argmax_accept(b, amax, alen, tok, nodes)
+
+
+def test_mask_discriminating_case(torch_cuda):
+    rng = np.random.Generator(np.random.PCG64(41))
+    parents = [random_tree(rng, 96, 8), random_tree(rng, 40)]
+    b = make_batch(parents=parents, prefix_lens=[24, 70], num_q_heads=8, num_kv_heads=2,
+                   head_dim=128, dtype="bf16", vocab=64, seed=41, qkv_std=1.0)
+    vt = bf16_bits_to_f32(b.v_tree) * 0.25 + 1.0       # tree values offset from the prefix's
+    b.v_tree = f32_to_bf16_bits(vt)
+    _, (out, *_rest) = run_device(b)
+    err = check_attention(b, out)
+    # the answer if every node could see every tree node of its request
+    far = 0.0
+    for r in range(b.num_requests):
+        a, e = int(b.node_indptr[r]), int(b.node_indptr[r + 1])
+        L = int(b.prefix_len[r])
+        pages = b.block_table[r, :(L + 15) // 16]
+        kp = bf16_bits_to_f32(b.k_pages[pages]).transpose(1, 0, 2, 3).reshape(2, -1, 128)[:, :L]
+        vp = bf16_bits_to_f32(b.v_pages[pages]).transpose(1, 0, 2, 3).reshape(2, -1, 128)[:, :L]
+        k = np.concatenate([kp, bf16_bits_to_f32(b.k_tree[a:e]).transpose(1, 0, 2)], 1).astype(np.float64)
+        v = np.concatenate([vp, bf16_bits_to_f32(b.v_tree[a:e]).transpose(1, 0, 2)], 1).astype(np.float64)
+        qh = bf16_bits_to_f32(b.q[a:e]).astype(np.float64)            # [n, 8, D]
+        kk = np.repeat(k, 4, axis=0)
+        vv = np.repeat(v, 4, axis=0)
+        s = np.einsum("nhd,hkd->nhk", qh, kk) * b.sm_scale
+        p = np.exp(s - s.max(-1, keepdims=True))
+        p /= p.sum(-1, keepdims=True)
+        unmasked = np.einsum("nhk,hkd->nhd", p, vv)
+        far = max(far, float(np.abs(out[a:e] - unmasked).max()))
+    assert far >= 10 * err, (far, err)
+
+
+@pytest.mark.parametrize("dtype,vocab,pad", [("bf16", 128256, 0), ("bf16", 3001, 2),
+                                             ("f32", 1024, 0), ("f32", 777, 3), ("bf16", 5, 0),
+                                             ("bf16", 1, 0)])
+def test_argmax_ties_and_alignment(torch_cuda, dtype, vocab, pad):
+    import torch
+    import paper_2501_12162_amd as ada
+    from paper_2501_12162_amd.device import to_device
+    rng = np.random.Generator(np.random.PCG64(vocab + pad))
+    logits, pos = make_tie_logits(rng, 97, vocab, dtype=dtype, max_ties=min(6, vocab), row_pad=pad)
+    dev = to_device(logits, dtype, "cuda")
+    out = torch.empty(97, dtype=torch.int32, device="cuda")
+    ada.adaserve_node_argmax(dev, vocab, out)
+    got = out.cpu().numpy()
+    np.testing.assert_array_equal(got, oracle.node_argmax(logits, vocab, dtype))
+    np.testing.assert_array_equal(got, [int(np.min(p)) for p in pos])
+
+
+def _accept_on_device(indptr, parent, draft, amax, max_accept):
+    import torch
+    import paper_2501_12162_amd as ada
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+    B = len(indptr) - 1
+    alen = torch.empty(B, dtype=torch.int32, device="cuda")
+    tok = torch.empty(B, max_accept, dtype=torch.int32, device="cuda")
+    nodes = torch.empty(B, max_accept, dtype=torch.int32, device="cuda")
+    ada.adaserve_tree_accept(node_indptr=t(indptr), parent=t(parent), draft_tokens=t(draft),
+                             target_argmax=t(amax), max_accept=max_accept, accept_len=alen,
+                             accept_tokens=tok, accept_nodes=nodes)
+    return alen.cpu().numpy(), tok.cpu().numpy(), nodes.cpu().numpy()
+
+
+def test_accept_exhaustive_small_trees(torch_cuda):
+    from test_oracle_accept import _exhaustive_batch
+    indptr, parent, draft, amax = _exhaustive_batch(7)
+    got = _accept_on_device(indptr, parent, draft, amax, 8)
+    ref = oracle.tree_accept(indptr, parent, draft, amax, 8)
+    for x, y in zip(got, ref):
+        np.testing.assert_array_equal(x, y)
+
+
+@pytest.mark.parametrize("max_accept", [128, 70, 9])
+def test_accept_large_trees_chains_and_depth_limit(torch_cuda, max_accept):
+    rng = np.random.Generator(np.random.PCG64(max_accept))
+    parents = [random_tree(rng, int(rng.integers(1, 129))) for _ in range(300)]
+    parents += [chain_tree(128), chain_tree(128), chain_tree(1), chain_tree(64)]
+    indptr = np.concatenate([[0], np.cumsum([len(p) for p in parents])]).astype(np.int32)
+    parent = np.concatenate(parents)
+    T = int(indptr[-1])
+    amax = rng.integers(0, 2, size=T).astype(np.int32)
+    draft = rng.integers(0, 2, size=T).astype(np.int32)
+    # make the two long chains match all the way down
+    for r in (300, 301):
+        a = indptr[r]
+        draft[a + 1:a + 128] = amax[a:a + 127]
+    got = _accept_on_device(indptr, parent, draft, amax, max_accept)
+    ref = oracle.tree_accept(indptr, parent, draft, amax, max_accept)
+    for x, y in zip(got, ref):
+        np.testing.assert_array_equal(x, y)
+    if max_accept == 128:
+        assert got[0][300] == 128
+
+
+def test_accept_malformed_trees(torch_cuda):
+    ptr = np.array([0, 3, 6, 10, 11, 11, 140], np.int32)
+    parent = np.concatenate([[-1, 2, 0], [0, 0, 1], [-1, 0, 1, 2], [-1], np.arange(-1, 128)]).astype(np.int32)
+    T = parent.size
+    draft = np.zeros(T, np.int32)
+    amax = np.zeros(T, np.int32)
+    got = _accept_on_device(ptr, parent, draft, amax, 3)
+    # child before parent; no root; too deep; fine; empty; 129 nodes
+    assert got[0].tolist() == [-1, -1, -1, 1, -1, -1]
+    ref = oracle.tree_accept(ptr[:5], parent[:11], draft[:11], amax[:11], 3)
+    for x, y in zip(got, ref):
+        np.testing.assert_array_equal(x[:4], y[:4])
+
+
+def test_empty_calls_are_noops(torch_cuda):
+    import torch
+    import paper_2501_12162_amd as ada
+    out = torch.empty(0, dtype=torch.int32, device="cuda")
+    ada.adaserve_node_argmax(torch.empty(0, 8, dtype=torch.bfloat16, device="cuda"), 8, out)
+    torch.cuda.synchronize()
+
+
+def test_native_library_is_the_in_tree_build(torch_cuda):
+    import os
+    import paper_2501_12162_amd as ada
+    with open("/proc/self/maps") as f:
+        maps = f.read()
+    assert os.path.realpath(ada.library_path()) in maps
