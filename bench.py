@@ -1,0 +1,258 @@
+#!/usr/bin/env python3
+"""Benchmark: verified tree tokens/s of one batched tree-verification pass on
+one MI355X, with the dominant kernel's roofline and the CPU oracle's rate.
+
+A step is one full verification pass over one batch: paged tree attention
+(+ split-KV combine), per-node argmax over the vocabulary, acceptance.
+Inputs are seeded synthetic tensors shaped like the workload named by
+``--workload`` (default: the Llama-3-8B-shaped batch), resident in device
+memory before timing starts.  Consecutive steps cycle through several
+copies of the inputs so that no step finds its K/V or logits in the 256 MB
+last-level (MALL) cache left behind by the previous one.
+
+Prints ONE JSON line on stdout.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense
+FP32_PEAK_TFLOPS = 157.3
+METRIC = "verified tree tokens/sec + % peak HBM GB/s, tree-verify attention, 1 MI355X"
+MALL_BYTES = 256 << 20
+
+
+def parse_args():
+    p = argparse.ArgumentParser(description=__doc__)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5],
+                   help="1 tiny-f32, 2 llama3-8b (default), 3 mixed-slo, 4 70b-shape, 5 long-context")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="approximate CPU time budget of the oracle baseline sample")
+    return p.parse_args()
+
+
+def algorithmic_costs(b):
+    """Bytes and flops the method must move / compute, per step."""
+    import numpy as np
+    s = b.elem_bytes
+    Hq, Hkv, D = b.num_q_heads, b.num_kv_heads, b.head_dim
+    n = b.tree_sizes().astype(np.int64)
+    L = b.prefix_len.astype(np.int64)
+    # depth of every node (for the tree part of the flop count)
+    depth_sum = 0
+    for r in range(b.num_requests):
+        par = b.request_parents(r)
+        dep = np.zeros(len(par), np.int64)
+        for i in range(1, len(par)):
+            dep[i] = dep[par[i]] + 1
+        depth_sum += int((dep + 1).sum())
+    attn_bytes = int((2 * L * Hkv * D * s).sum() + (n * (2 * Hq + 2 * Hkv) * D * s).sum()
+                     + 4 * ((L + 15) // 16).sum() + 4 * n.sum() + 8 * b.num_requests)
+    attn_flops = int((4 * D * Hq * n * L).sum()) + 4 * D * Hq * depth_sum
+    argmax_bytes = int(b.total_nodes) * b.vocab * s + 4 * int(b.total_nodes)
+    accept_bytes = 16 * int(b.total_nodes)
+    return dict(attn_bytes=attn_bytes, attn_flops=attn_flops, argmax_bytes=argmax_bytes,
+                accept_bytes=accept_bytes)
+
+
+def make_replicas(dev, count):
+    """``count`` device copies of the per-step input tensors (copy 0 = originals)."""
+    reps = [dict(q=dev.q, k_tree=dev.k_tree, v_tree=dev.v_tree, k_pages=dev.k_pages,
+                 v_pages=dev.v_pages, logits=dev.logits)]
+    for _ in range(count - 1):
+        reps.append({k: v.clone() for k, v in reps[0].items()})
+    return reps
+
+
+def cpu_baseline(b, budget_s):
+    """The oracle (untuned) on a bounded sample of the same workload."""
+    import numpy as np
+    import oracle
+    threads = oracle.num_threads()
+    T = b.total_nodes
+    # cost estimate: multiply-adds of the attention per node
+    macs_per_node = 2.0 * b.num_q_heads * b.head_dim * (float(b.prefix_len.mean()) + 8.0)
+    probe = min(T, 8)
+    nodes_all = np.arange(T)
+    t0 = time.perf_counter()
+    oracle.tree_attn_batch(b, nodes=nodes_all[:probe])
+    per_node = max((time.perf_counter() - t0) / probe, 1e-6)
+    want = int(min(T, max(1, budget_s / per_node)))
+    # an even spread of nodes over the whole batch
+    sel = np.unique(np.linspace(0, T - 1, want).round().astype(np.int64))
+    t0 = time.perf_counter()
+    oracle.tree_attn_batch(b, nodes=sel)
+    amax = oracle.node_argmax(b.logits, b.vocab, b.dtype, rows=sel)
+    t_attn_argmax = time.perf_counter() - t0
+    full_amax = b.planted_argmax  # acceptance timing needs a full argmax vector
+    t0 = time.perf_counter()
+    oracle.tree_accept(b.node_indptr, b.parent, b.draft_tokens, full_amax, 128)
+    t_accept = time.perf_counter() - t0
+    per_node_s = t_attn_argmax / sel.size + t_accept / T
+    return {
+        "value": 1.0 / per_node_s,
+        "unit": "tree tokens/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": ("%d of %d tree nodes (attention over all q-heads + vocab argmax of their rows, "
+                   "evenly spread over the batch) plus acceptance of the whole batch; fp64; "
+                   "%.1f s wall" % (sel.size, T, t_attn_argmax + t_accept)),
+        "macs_per_node_est": macs_per_node,
+    }
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the tree-verification path is not sharded "
+              "across GPUs here (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2501_12162_amd as ada
+    from paper_2501_12162_amd.device import DeviceBatch
+    from paper_2501_12162_amd.workload import WORKLOAD_NAMES, make_config
+
+    if not os.path.exists(ada.library_path()):
+        from paper_2501_12162_amd.build import build
+        build()
+    ada.load_library()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev_name = torch.cuda.get_device_name(0)
+
+    b = make_config(args.workload)
+    costs = algorithmic_costs(b)
+    dev = DeviceBatch(b)
+    step_bytes = sum(t.numel() * t.element_size() for t in
+                     (dev.q, dev.k_tree, dev.v_tree, dev.k_pages, dev.v_pages, dev.logits))
+    n_rep = max(2, math.ceil(3 * MALL_BYTES / step_bytes) + 1)
+    reps = make_replicas(dev, n_rep)
+    stream = torch.cuda.current_stream()
+
+    def run_step(i, ev=None):
+        rp = reps[i % n_rep]
+        if ev is not None:
+            ev[0].record(stream)
+        ada.adaserve_tree_attn_verify(
+            node_indptr=dev.node_indptr, node_indptr_host=dev.node_indptr_host, parent=dev.parent,
+            q=rp["q"], k_tree=rp["k_tree"], v_tree=rp["v_tree"], k_pages=rp["k_pages"],
+            v_pages=rp["v_pages"], block_table=dev.block_table, prefix_len=dev.prefix_len,
+            prefix_len_host=dev.prefix_len_host, sm_scale=b.sm_scale, out=dev.out,
+            workspace=dev.workspace)
+        if ev is not None:
+            ev[1].record(stream)
+        ada.adaserve_node_argmax(rp["logits"], b.vocab, dev.target_argmax)
+        if ev is not None:
+            ev[2].record(stream)
+        ada.adaserve_tree_accept(node_indptr=dev.node_indptr, parent=dev.parent,
+                                 draft_tokens=dev.draft_tokens, target_argmax=dev.target_argmax,
+                                 max_accept=dev.max_accept, accept_len=dev.accept_len,
+                                 accept_tokens=dev.accept_tokens, accept_nodes=dev.accept_nodes)
+        if ev is not None:
+            ev[3].record(stream)
+
+    # calibration copy of a known size (reference for HBM byte counters)
+    calib_src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda").fill_(1)
+    calib_dst = torch.empty_like(calib_src)
+    calib_dst.copy_(calib_src)
+
+    for i in range(args.warmup):
+        run_step(i)
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        run_step(args.warmup + i, events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    attn_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
+    argmax_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
+    accept_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
+
+    # sanity: the last step's argmax must equal the planted maxima
+    got = dev.target_argmax.cpu().numpy()
+    if not np.array_equal(got, b.planted_argmax):
+        print("bench.py: argmax mismatch, results invalid", file=sys.stderr)
+        sys.exit(3)
+    alen = dev.accept_len.cpu().numpy()
+
+    T = b.total_nodes
+    ms_per_step = wall * 1e3 / args.steps
+    value = T * args.steps / wall
+    attn_us, argmax_us, accept_us = (float(x.mean()) * 1e3 for x in (attn_ms, argmax_ms, accept_ms))
+    attn_gbs = costs["attn_bytes"] / (attn_us * 1e-6) / 1e9
+    argmax_gbs = costs["argmax_bytes"] / (argmax_us * 1e-6) / 1e9
+    attn_tflops = costs["attn_flops"] / (attn_us * 1e-6) / 1e12
+    is_bf16 = b.dtype == "bf16"
+    mfma_peak = BF16_MFMA_PEAK_TFLOPS if is_bf16 else FP32_PEAK_TFLOPS
+    ridge = mfma_peak * 1e12 / (HBM_PEAK_GBS * 1e9)
+    attn_ai = costs["attn_flops"] / costs["attn_bytes"]
+    if attn_us >= argmax_us:
+        if attn_ai > ridge:
+            roof = {"kernel": "tree_attn", "bound": "mfma", "achieved": attn_tflops, "peak": mfma_peak,
+                    "unit": "TFLOP/s", "frac": attn_tflops / mfma_peak}
+        else:
+            roof = {"kernel": "tree_attn", "bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS}
+    else:
+        roof = {"kernel": "node_argmax", "bound": "hbm", "achieved": argmax_gbs, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": argmax_gbs / HBM_PEAK_GBS}
+    roof["traffic"] = None
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tree tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if is_bf16 else "f32",
+        "data": "synthetic (seeded; shapes of the named workload)",
+        "config": {
+            "workload": WORKLOAD_NAMES[args.workload],
+            "requests": b.num_requests,
+            "tree_tokens": T,
+            "prefix_tokens": int(b.prefix_len.sum()),
+            "q_heads": b.num_q_heads, "kv_heads": b.num_kv_heads, "head_dim": b.head_dim,
+            "page_size": b.page_size, "vocab": b.vocab,
+            "input_copies": n_rep,
+        },
+        "roofline": roof,
+        "kernels": {
+            "tree_attn_us": attn_us, "tree_attn_hbm_frac": attn_gbs / HBM_PEAK_GBS,
+            "tree_attn_mfma_frac": attn_tflops / mfma_peak, "tree_attn_ai_flop_per_byte": attn_ai,
+            "tree_attn_alg_bytes": costs["attn_bytes"], "tree_attn_alg_flops": costs["attn_flops"],
+            "node_argmax_us": argmax_us, "node_argmax_hbm_frac": argmax_gbs / HBM_PEAK_GBS,
+            "node_argmax_alg_bytes": costs["argmax_bytes"],
+            "tree_accept_us": accept_us,
+            "step_event_sum_us": attn_us + argmax_us + accept_us,
+        },
+        "accepted_tokens_per_step": int(alen.sum()),
+        "accepted_tokens_per_s": float(alen.sum()) * args.steps / wall,
+        "device": dev_name,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

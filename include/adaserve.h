@@ -102,7 +102,10 @@ size_t adaserve_tree_attn_workspace_bytes(int32_t num_requests, const int32_t *n
  * into the result (they may hold NaN).  Block-table entries outside
  * [0, num_pages) are treated as all-zero pages.  The device arrays must equal
  * their host mirrors.  workspace must hold at least
- * adaserve_tree_attn_workspace_bytes(...) bytes (256-byte aligned).
+ * adaserve_tree_attn_workspace_bytes(...) bytes (256-byte aligned; contents
+ * need no initialisation); calls that share a workspace must not overlap in
+ * time.  When some prefix is split, a second kernel (the split-KV merge) is
+ * enqueued after the attention kernel on the same stream.
  */
 int32_t adaserve_tree_attn_verify(int32_t num_requests, const int32_t *node_indptr,
                                   const int32_t *node_indptr_host, const int32_t *parent,

@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <algorithm>
 #include <mutex>
 #include <string>
 
@@ -91,6 +92,7 @@ int32_t validate_attn_shape(int32_t num_requests, const int32_t *indptr_host, co
     total += n;
     const int32_t L = plen_host[r];
     if (L < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "prefix_len[%d] = %d < 0", r, L);
+    if (L >= (1 << 23)) return fail(ADASERVE_ERR_UNSUPPORTED, "prefix_len[%d] = %d (max %d)", r, L, (1 << 23) - 1);
     if (bt_stride_or_neg >= 0 && ceil_div(L, kPageSize) > bt_stride_or_neg)
       return fail(ADASERVE_ERR_INVALID_ARGUMENT, "prefix_len[%d] = %d needs %d pages > block_table_stride %d", r, L,
                   ceil_div(L, kPageSize), bt_stride_or_neg);
@@ -101,47 +103,106 @@ int32_t validate_attn_shape(int32_t num_requests, const int32_t *indptr_host, co
 }
 
 struct AttnPlan {
-  int32_t chunk_keys = 0;
+  int32_t rows_per_tile = 0;
+  int32_t chunk_target = 0;
   int64_t units = 0;
   int64_t padded_grid = 0;
   int64_t row_groups = 0;
   bool needs_combine = false;
   size_t ws_o_bytes = 0;
+  size_t ws_ml_bytes = 0;
   size_t ws_bytes = 0;
 };
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Split-KV plan.  Chooses the prefix chunk (a power of two between 256 and
-// 8192 keys) so that the batch has about 1024 work units: enough to keep
-// 256 CUs busy with two resident workgroups each while leaving partials
-// rare.  Depends only on host-visible sizes.
+int64_t count_units(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
+                    int32_t group, int32_t rows_per_tile, int32_t chunk_target) {
+  int64_t u = 0;
+  for (int32_t r = 0; r < B; ++r)
+    u += request_units(indptr_host[r + 1] - indptr_host[r], plen_host[r], hkv, group, rows_per_tile,
+                       chunk_target);
+  return u;
+}
+
+// Work plan of the bf16 kernel, from host-visible sizes only.
+//  * Row tiles of 128 rows unless that leaves fewer (request, kv-head, tile)
+//    groups than CUs and no prefix would need splitting; then 64-row tiles
+//    (the tiles of one group re-read the same KV from their XCD's L2).
+//  * The batch-wide chunk target is the largest power of two in
+//    [kMinChunk, kMaxChunk] that still yields kTargetUnits work units (about
+//    four per CU: two resident per CU, two waves of them for balance).
+//    chunk_keys() keeps every request's chunk at >= 32 rows so that split
+//    partials stay under 1/16 of the KV traffic.
+//  * Requests are dispatched in descending order of per-unit cost (keys x
+//    rows), so the longest units start first and the tail stays short.
 AttnPlan make_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
                    int32_t group, int32_t head_dim, int32_t dtype) {
+  constexpr int64_t kCUs = 256, kTargetUnits = 1024;
   AttnPlan p;
   if (dtype != ADASERVE_BF16 || B == 0) return p;
-  int64_t work = 0;
+  int64_t groups128 = 0, groups64 = 0;
+  int32_t max_len = 0;
   for (int32_t r = 0; r < B; ++r) {
     const int32_t n = indptr_host[r + 1] - indptr_host[r];
-    work += (int64_t)hkv * row_tiles(n, group) * (int64_t)(plen_host[r] > 0 ? plen_host[r] : 1);
+    groups128 += (int64_t)hkv * row_tiles(n, group, 128);
+    groups64 += (int64_t)hkv * row_tiles(n, group, 64);
+    max_len = std::max(max_len, plen_host[r]);
   }
-  const int64_t target_units = 1024;
-  int32_t chunk = 256;
-  while (chunk < 8192 && (int64_t)chunk * target_units < work) chunk *= 2;
-  p.chunk_keys = chunk;
+  p.rows_per_tile = (groups128 < kCUs && groups64 >= kCUs) ? 64 : 128;
+  p.chunk_target = kMinChunk;
+  for (int32_t c = kMaxChunk; c >= kMinChunk; c /= 2) {
+    if (count_units(B, indptr_host, plen_host, hkv, group, p.rows_per_tile, c) >= kTargetUnits) {
+      p.chunk_target = c;
+      break;
+    }
+  }
+  if (p.rows_per_tile == 64) p.chunk_target = kMaxChunk;  // 64-row tiles never split
   for (int32_t r = 0; r < B; ++r) {
     const int32_t n = indptr_host[r + 1] - indptr_host[r];
-    const int32_t c = prefix_chunks(plen_host[r], chunk);
-    p.units += request_units(n, plen_host[r], hkv, group, chunk);
-    p.row_groups += (int64_t)hkv * row_tiles(n, group);
-    if (c > 1) p.needs_combine = true;
+    p.row_groups += (int64_t)hkv * row_tiles(n, group, p.rows_per_tile);
+    if (prefix_chunks(plen_host[r], chunk_keys(n, group, p.rows_per_tile, p.chunk_target)) > 1)
+      p.needs_combine = true;
   }
+  p.units = count_units(B, indptr_host, plen_host, hkv, group, p.rows_per_tile, p.chunk_target);
   p.padded_grid = pad_to_xcds(p.units);
   if (p.needs_combine) {
-    p.ws_o_bytes = round_up((size_t)p.units * kRowsPerTile * head_dim * sizeof(float), 256);
-    p.ws_bytes = p.ws_o_bytes + round_up((size_t)p.units * kRowsPerTile * 2 * sizeof(float), 256);
+    p.ws_o_bytes = round_up((size_t)p.units * kMaxRowsPerTile * head_dim * sizeof(float), 256);
+    p.ws_ml_bytes = round_up((size_t)p.units * kMaxRowsPerTile * 2 * sizeof(float), 256);
+    p.ws_bytes = p.ws_o_bytes + p.ws_ml_bytes;
   }
   return p;
+}
+
+// Fills the dispatch-ordered request table (descending per-unit cost) when
+// the batch fits in the kernel arguments; otherwise leaves it empty.
+void fill_plan_table(TreeAttnArgs &a, int32_t B, const int32_t *indptr_host, const int32_t *plen_host,
+                     const AttnPlan &p) {
+  a.plan_count = 0;
+  if (B > kPlanMax) return;
+  int32_t order[kPlanMax];
+  int64_t cost[kPlanMax];
+  for (int32_t r = 0; r < B; ++r) {
+    const int32_t n = indptr_host[r + 1] - indptr_host[r];
+    const int32_t rows = std::min(n * a.group, p.rows_per_tile);
+    const int32_t keys = std::min(std::max(plen_host[r], 0), chunk_keys(n, a.group, p.rows_per_tile, p.chunk_target));
+    cost[r] = (int64_t)(keys + n) * rows;
+    order[r] = r;
+  }
+  std::stable_sort(order, order + B, [&](int32_t x, int32_t y) { return cost[x] > cost[y]; });
+  int64_t end = 0, gend = 0;
+  for (int32_t i = 0; i < B; ++i) {
+    const int32_t r = order[i];
+    const int32_t n = indptr_host[r + 1] - indptr_host[r];
+    end += request_units(n, plen_host[r], a.num_kv_heads, a.group, p.rows_per_tile, p.chunk_target);
+    gend += (int64_t)a.num_kv_heads * row_tiles(n, a.group, p.rows_per_tile);
+    a.plan[i].unit_end = (int32_t)end;
+    a.plan[i].group_end = (int32_t)gend;
+    a.plan[i].request = r;
+    a.plan[i].node_base = indptr_host[r];
+    a.plan[i].n_and_len = n | (plen_host[r] << 8);
+  }
+  a.plan_count = B;
 }
 
 }  // namespace
@@ -221,7 +282,9 @@ int32_t adaserve_tree_attn_verify(int32_t num_requests, const int32_t *node_indp
   a.num_q_heads = num_q_heads;
   a.num_kv_heads = num_kv_heads;
   a.group = shape.group;
-  a.chunk_keys = plan.chunk_keys;
+  a.rows_per_tile = plan.rows_per_tile;
+  a.chunk_target = plan.chunk_target;
+  if (dtype == ADASERVE_BF16) fill_plan_table(a, num_requests, node_indptr_host, prefix_len_host, plan);
   a.units = plan.units;
   a.padded_grid = plan.padded_grid;
   a.row_groups = plan.row_groups;

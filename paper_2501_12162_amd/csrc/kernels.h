@@ -6,6 +6,18 @@
 
 namespace adaserve {
 
+// Requests in descending order of per-unit cost, carried in the kernel
+// arguments so a workgroup finds its unit without touching memory.  Batches
+// with more requests fall back to a scan of node_indptr / prefix_len.
+constexpr int kPlanMax = 160;
+struct PlanEntry {
+  int32_t unit_end;   // exclusive end of this request's units in dispatch order
+  int32_t group_end;  // exclusive end of its (kv-head, row tile) groups, same order
+  int32_t request;
+  int32_t node_base;  // node_indptr[request]
+  int32_t n_and_len;  // tree nodes (bits 0..7) | prefix length << 8
+};
+
 struct TreeAttnArgs {
   const int32_t *node_indptr;  // [B+1]
   const int32_t *parent;       // [T] local ids
@@ -18,24 +30,27 @@ struct TreeAttnArgs {
   const void *v_tree;
   const void *k_pages;         // [num_pages, Hkv, 16, D]
   const void *v_pages;
+  const void *zero16;          // 16 zero bytes in device memory (source of masked DMA lanes)
   void *out;                   // [T, Hq, D]
-  float *ws_o;                 // [units, kRowsPerTile, D] partial numerators
-  float *ws_ml;                // [units, kRowsPerTile, 2]  (running max in log2 units, denominator)
+  float *ws_o;                 // [units, kMaxRowsPerTile, D] partial numerators
+  float *ws_ml;                // [units, kMaxRowsPerTile, 2]  (reference max in raw units, denominator)
   int32_t num_requests;
   int32_t total_nodes;
   int32_t num_q_heads;
   int32_t num_kv_heads;
   int32_t group;               // Hq / Hkv
-  int32_t chunk_keys;          // prefix keys per unit (multiple of the key block)
+  int32_t rows_per_tile;       // 64 or 128
+  int32_t chunk_target;        // batch-wide prefix chunk (see chunk_keys() in plan.h)
   int64_t units;               // work units in the batch
   int64_t padded_grid;         // units rounded up to the XCD count
   int64_t row_groups;          // sum over requests of Hkv * row tiles
   float sm_scale;
   float scale_log2;            // sm_scale * log2(e)
+  int32_t plan_count;          // entries used in plan[] (0: scan the device arrays)
+  PlanEntry plan[kPlanMax];
 };
 
-hipError_t launch_tree_attn_bf16(const TreeAttnArgs &a, int head_dim, bool needs_combine,
-                                 hipStream_t stream);
+hipError_t launch_tree_attn_bf16(TreeAttnArgs &a, int head_dim, bool needs_combine, hipStream_t stream);
 hipError_t launch_tree_attn_f32(const TreeAttnArgs &a, int head_dim, hipStream_t stream);
 
 hipError_t launch_node_argmax(const void *logits, int64_t row_stride, int32_t rows, int32_t vocab,

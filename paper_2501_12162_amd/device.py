@@ -52,7 +52,7 @@ class DeviceBatch:
                                                 batch.num_q_heads, batch.num_kv_heads,
                                                 batch.head_dim, batch.page_size, self.dtype_code)
         self.workspace_bytes = ws
-        self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=device) if ws else None
+        self.workspace = torch.zeros(max(ws, 256), dtype=torch.uint8, device=device) if ws else None
         self.max_accept = int(max_accept)
         self.target_argmax = torch.empty(T, dtype=torch.int32, device=device)
         self.accept_len = torch.empty(B, dtype=torch.int32, device=device)
