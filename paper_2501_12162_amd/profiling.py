@@ -1,0 +1,122 @@
+"""Summaries of rocprofv3 output for the committed profiles.
+
+Usage (on the GPU machine, after the runs named in each summary's header):
+
+  python -m paper_2501_12162_amd.profiling stats  <kernel_stats.csv> <out.md> "<command>"
+  python -m paper_2501_12162_amd.profiling traffic <fetch_dir> <write_dir> <workload> <out.json> "<commands>"
+
+``traffic`` reads the per-dispatch FETCH_SIZE and WRITE_SIZE counters (KiB) of
+the tree-attention and argmax kernels, scales each by the factor that makes
+the bench's calibration copy (a device-to-device copy of exactly 256 MiB,
+launched by bench.py before timing) read and write 256 MiB, and stores the
+result with a hash of the kernel sources; ``bench.py`` reports it only while
+the sources still have that hash.
+"""
+from __future__ import annotations
+
+import csv
+import glob
+import hashlib
+import json
+import os
+import statistics
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+CALIB_BYTES = 256 << 20
+
+
+def kernel_source_hash() -> str:
+    """sha256 over the HIP/C++ sources and internal headers of the library."""
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(PKG, "csrc", "*"))):
+        with open(p, "rb") as f:
+            h.update(os.path.basename(p).encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def kernel_kind(name: str) -> str:
+    if "tree_attn_combine" in name:
+        return "tree_attn_combine"
+    if "tree_attn_bf16" in name or "tree_attn_f32" in name:
+        return "tree_attn"
+    if "node_argmax" in name:
+        return "node_argmax"
+    if "tree_accept" in name:
+        return "tree_accept"
+    return "other"
+
+
+def stats_markdown(csv_path: str, command: str) -> str:
+    rows = list(csv.DictReader(open(csv_path)))
+    out = ["# rocprofv3 kernel statistics", "", "Command:", "", "```", command, "```", "",
+           "| kernel | calls | average (us) | min (us) | max (us) | share |", "|---|---|---|---|---|---|"]
+    for r in rows:
+        out.append("| %s | %s | %.2f | %.2f | %.2f | %.1f%% |" % (
+            r["Name"][:90].replace("|", "/"), r["Calls"], float(r["AverageNs"]) / 1e3,
+            float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
+    return "\n".join(out) + "\n"
+
+
+def _counter_rows(directory: str, counter: str):
+    files = glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True)
+    rows = []
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] == counter:
+                rows.append(r)
+    return rows
+
+
+def _calibration_factor(rows, expect_bytes: int) -> float:
+    # bench.py launches the calibration copy right before its first
+    # verification step: it is the last non-library dispatch before the first
+    # tree-attention dispatch.
+    rows = sorted(rows, key=lambda r: int(r["Dispatch_Id"]))
+    first = min(int(r["Dispatch_Id"]) for r in rows if kernel_kind(r["Kernel_Name"]) == "tree_attn")
+    before = [r for r in rows if int(r["Dispatch_Id"]) < first and kernel_kind(r["Kernel_Name"]) == "other"]
+    if not before:
+        raise RuntimeError("calibration copy not found")
+    value = float(before[-1]["Counter_Value"])
+    return (expect_bytes / 1024.0) / value
+
+
+def traffic_summary(fetch_dir: str, write_dir: str, workload: int, commands: str) -> dict:
+    fetch = _counter_rows(fetch_dir, "FETCH_SIZE")
+    write = _counter_rows(write_dir, "WRITE_SIZE")
+    f_factor = _calibration_factor(fetch, CALIB_BYTES)
+    w_factor = _calibration_factor(write, CALIB_BYTES)
+    res = {"workload": workload, "kernel_source_sha": kernel_source_hash(),
+           "fetch_factor": f_factor, "write_factor": w_factor, "commands": commands, "kernels": {}}
+    for kind in ("tree_attn", "tree_attn_combine", "node_argmax", "tree_accept"):
+        fv = [float(r["Counter_Value"]) for r in fetch if kernel_kind(r["Kernel_Name"]) == kind]
+        wv = [float(r["Counter_Value"]) for r in write if kernel_kind(r["Kernel_Name"]) == kind]
+        if not fv:
+            continue
+        fb = statistics.median(fv) * 1024 * f_factor
+        wb = statistics.median(wv) * 1024 * w_factor if wv else 0.0
+        res["kernels"][kind] = {"fetch_bytes": fb, "write_bytes": wb, "bytes": fb + wb,
+                                "dispatches": len(fv)}
+    return res
+
+
+def main(argv):
+    if len(argv) >= 4 and argv[1] == "stats":
+        md = stats_markdown(argv[2], argv[4] if len(argv) > 4 else "")
+        with open(argv[3], "w") as f:
+            f.write(md)
+        print(md)
+    elif len(argv) >= 6 and argv[1] == "traffic":
+        res = traffic_summary(argv[2], argv[3], int(argv[4]), argv[6] if len(argv) > 6 else "")
+        with open(argv[5], "w") as f:
+            json.dump(res, f, indent=1)
+        print(json.dumps(res, indent=1))
+    else:
+        print(__doc__)
+        return 2
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main(sys.argv))
