@@ -105,6 +105,7 @@ int32_t validate_attn_shape(int32_t num_requests, const int32_t *indptr_host, co
 struct AttnPlan {
   int32_t rows_per_tile = 0;
   int32_t chunk_target = 0;
+  int32_t chunk_floor = 0;
   int64_t units = 0;
   int64_t padded_grid = 0;
   int64_t row_groups = 0;
@@ -112,59 +113,59 @@ struct AttnPlan {
   size_t ws_o_bytes = 0;
   size_t ws_ml_bytes = 0;
   size_t ws_bytes = 0;
+  double est_us = 0.0;
 };
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-int64_t count_units(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
-                    int32_t group, int32_t rows_per_tile, int32_t chunk_target) {
-  int64_t u = 0;
-  for (int32_t r = 0; r < B; ++r)
-    u += request_units(indptr_host[r + 1] - indptr_host[r], plen_host[r], hkv, group, rows_per_tile,
-                       chunk_target);
-  return u;
-}
+// Throughput figures the planner's cost model uses, measured on MI355X:
+// paged K/V streaming over the whole chip, one workgroup's streaming rate
+// with three 16 KB blocks in flight, the attention loop's compute time per
+// 32-key block of a full 128-row tile (two workgroups sharing a CU), and
+// the gap a second (combine) kernel adds.
+constexpr double kChipBytesPerUs = 6.0e6;
+constexpr double kWgBytesPerUs = 1.9e4;
+constexpr double kBlockComputeUs = 1.14;
+constexpr double kCombineGapUs = 3.0;
+constexpr int kCUs = 256;
 
-// Work plan of the bf16 kernel, from host-visible sizes only.
-//  * Row tiles of 128 rows unless that leaves fewer (request, kv-head, tile)
-//    groups than CUs and no prefix would need splitting; then 64-row tiles
-//    (the tiles of one group re-read the same KV from their XCD's L2).
-//  * The batch-wide chunk target is the largest power of two in
-//    [kMinChunk, kMaxChunk] that still yields kTargetUnits work units (about
-//    four per CU: two resident per CU, two waves of them for balance).
-//    chunk_keys() keeps every request's chunk at >= 32 rows so that split
-//    partials stay under 1/16 of the KV traffic.
-//  * Requests are dispatched in descending order of per-unit cost (keys x
-//    rows), so the longest units start first and the tail stays short.
-AttnPlan make_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
-                   int32_t group, int32_t head_dim, int32_t dtype) {
-  constexpr int64_t kCUs = 256, kTargetUnits = 1024;
+// Plan for one (row tile, chunk target, chunk floor) choice, with its cost
+// estimate: the larger of the chip-wide streaming time and the longest unit
+// (whose stream and compute overlap), plus the combine pass when a prefix
+// is split.
+AttnPlan evaluate_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
+                       int32_t group, int32_t head_dim, int32_t rows_per_tile, int32_t chunk_target,
+                       int32_t floor_mult) {
   AttnPlan p;
-  if (dtype != ADASERVE_BF16 || B == 0) return p;
-  int64_t groups128 = 0, groups64 = 0;
-  int32_t max_len = 0;
+  p.rows_per_tile = rows_per_tile;
+  p.chunk_target = chunk_target;
+  p.chunk_floor = floor_mult;
+  const double key_bytes = 4.0 * head_dim;  // bf16 K and V of one key of one kv-head
+  double kv_bytes = 0, partial_bytes = 0, longest = 0, work = 0;
   for (int32_t r = 0; r < B; ++r) {
     const int32_t n = indptr_host[r + 1] - indptr_host[r];
-    groups128 += (int64_t)hkv * row_tiles(n, group, 128);
-    groups64 += (int64_t)hkv * row_tiles(n, group, 64);
-    max_len = std::max(max_len, plen_host[r]);
-  }
-  p.rows_per_tile = (groups128 < kCUs && groups64 >= kCUs) ? 64 : 128;
-  p.chunk_target = kMinChunk;
-  for (int32_t c = kMaxChunk; c >= kMinChunk; c /= 2) {
-    if (count_units(B, indptr_host, plen_host, hkv, group, p.rows_per_tile, c) >= kTargetUnits) {
-      p.chunk_target = c;
-      break;
-    }
-  }
-  if (p.rows_per_tile == 64) p.chunk_target = kMaxChunk;  // 64-row tiles never split
-  for (int32_t r = 0; r < B; ++r) {
-    const int32_t n = indptr_host[r + 1] - indptr_host[r];
-    p.row_groups += (int64_t)hkv * row_tiles(n, group, p.rows_per_tile);
-    if (prefix_chunks(plen_host[r], chunk_keys(n, group, p.rows_per_tile, p.chunk_target)) > 1)
+    const int32_t L = plen_host[r];
+    const int32_t tiles = row_tiles(n, group, rows_per_tile);
+    const int32_t ck = chunk_keys(n, group, rows_per_tile, chunk_target, floor_mult);
+    const int32_t chunks = prefix_chunks(L, ck);
+    p.units += (int64_t)hkv * tiles * chunks;
+    p.row_groups += (int64_t)hkv * tiles;
+    kv_bytes += (double)hkv * (L + n) * key_bytes;
+    if (chunks > 1) {
       p.needs_combine = true;
+      partial_bytes += (double)hkv * chunks * n * group * (head_dim + 2) * 4.0;
+    }
+    const int32_t rows = std::min(n * group, rows_per_tile);
+    const double keys = std::min(L, ck) + n;
+    const double blocks = keys / 32.0;
+    const double t_unit = std::max(keys * key_bytes / kWgBytesPerUs,
+                                   blocks * kBlockComputeUs * std::max(rows, 32) / 128.0);
+    longest = std::max(longest, t_unit);
+    work += (double)hkv * tiles * chunks * t_unit;
   }
-  p.units = count_units(B, indptr_host, plen_host, hkv, group, p.rows_per_tile, p.chunk_target);
+  const double slots = 2.0 * kCUs;
+  const double t_main = std::max({(kv_bytes + partial_bytes) / kChipBytesPerUs, longest, work / slots});
+  p.est_us = t_main + (p.needs_combine ? kCombineGapUs + 2.0 * partial_bytes / kChipBytesPerUs : 0.0);
   p.padded_grid = pad_to_xcds(p.units);
   if (p.needs_combine) {
     p.ws_o_bytes = round_up((size_t)p.units * kMaxRowsPerTile * head_dim * sizeof(float), 256);
@@ -172,6 +173,27 @@ AttnPlan make_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_ho
     p.ws_bytes = p.ws_o_bytes + p.ws_ml_bytes;
   }
   return p;
+}
+
+// Work plan of the bf16 kernel, from host-visible sizes only: the cheapest
+// estimate over row tiles {64, 128}, chunk targets {256 .. 8192} and chunk
+// floors {8, 16, 32} keys per row (see evaluate_plan).  Requests are then
+// dispatched in descending order of per-unit cost (fill_plan_table).
+AttnPlan make_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
+                   int32_t group, int32_t head_dim, int32_t dtype) {
+  AttnPlan best;
+  if (dtype != ADASERVE_BF16 || B == 0) return best;
+  bool have = false;
+  for (int32_t rt : {128, 64})
+    for (int32_t fm : {32, 16, 8})
+      for (int32_t c = kMaxChunk; c >= kMinChunk; c /= 2) {
+        AttnPlan p = evaluate_plan(B, indptr_host, plen_host, hkv, group, head_dim, rt, c, fm);
+        if (!have || p.est_us < best.est_us * 0.98) {
+          best = p;
+          have = true;
+        }
+      }
+  return best;
 }
 
 // Fills the dispatch-ordered request table (descending per-unit cost) when
@@ -185,7 +207,8 @@ void fill_plan_table(TreeAttnArgs &a, int32_t B, const int32_t *indptr_host, con
   for (int32_t r = 0; r < B; ++r) {
     const int32_t n = indptr_host[r + 1] - indptr_host[r];
     const int32_t rows = std::min(n * a.group, p.rows_per_tile);
-    const int32_t keys = std::min(std::max(plen_host[r], 0), chunk_keys(n, a.group, p.rows_per_tile, p.chunk_target));
+    const int32_t keys = std::min(std::max(plen_host[r], 0),
+                                  chunk_keys(n, a.group, p.rows_per_tile, p.chunk_target, p.chunk_floor));
     cost[r] = (int64_t)(keys + n) * rows;
     order[r] = r;
   }
@@ -194,7 +217,8 @@ void fill_plan_table(TreeAttnArgs &a, int32_t B, const int32_t *indptr_host, con
   for (int32_t i = 0; i < B; ++i) {
     const int32_t r = order[i];
     const int32_t n = indptr_host[r + 1] - indptr_host[r];
-    end += request_units(n, plen_host[r], a.num_kv_heads, a.group, p.rows_per_tile, p.chunk_target);
+    end += request_units(n, plen_host[r], a.num_kv_heads, a.group, p.rows_per_tile, p.chunk_target,
+                         p.chunk_floor);
     gend += (int64_t)a.num_kv_heads * row_tiles(n, a.group, p.rows_per_tile);
     a.plan[i].unit_end = (int32_t)end;
     a.plan[i].group_end = (int32_t)gend;
@@ -284,6 +308,7 @@ int32_t adaserve_tree_attn_verify(int32_t num_requests, const int32_t *node_indp
   a.group = shape.group;
   a.rows_per_tile = plan.rows_per_tile;
   a.chunk_target = plan.chunk_target;
+  a.chunk_floor = plan.chunk_floor;
   if (dtype == ADASERVE_BF16) fill_plan_table(a, num_requests, node_indptr_host, prefix_len_host, plan);
   a.units = plan.units;
   a.padded_grid = plan.padded_grid;

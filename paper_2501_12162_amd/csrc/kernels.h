@@ -41,6 +41,7 @@ struct TreeAttnArgs {
   int32_t group;               // Hq / Hkv
   int32_t rows_per_tile;       // 64 or 128
   int32_t chunk_target;        // batch-wide prefix chunk (see chunk_keys() in plan.h)
+  int32_t chunk_floor;         // minimum chunk, in keys per tile row
   int64_t units;               // work units in the batch
   int64_t padded_grid;         // units rounded up to the XCD count
   int64_t row_groups;          // sum over requests of Hkv * row tiles

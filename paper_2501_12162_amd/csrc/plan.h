@@ -11,12 +11,12 @@
 // A split prefix costs fp32 partial results: per unit, rows * D * 4 bytes
 // written and read back against chunk * D * 4 bytes of bf16 K and V
 // streamed, i.e. a traffic ratio of about 2 * rows / chunk.  chunk_keys()
-// therefore never goes below 32 * rows (ratio <= 1/16); above that floor the
-// batch-wide `chunk_target` sets the split.
+// therefore never goes below `floor_mult` * rows keys (the planner picks 8,
+// 16 or 32); above that floor the batch-wide `chunk_target` sets the split.
 //
 // Units are numbered request by request; inside a request the order is
 // (g, chunk, tile) with the tile fastest, so the tiles that read the same KV
-// chunk are neighbours (and land on one XCD, see xcd_swizzle).
+// chunk are neighbours (and mostly land on one XCD, see xcd_swizzle).
 //
 // The host planner and the device-side unit lookup both use the functions
 // below, so their arithmetic cannot drift apart.
@@ -47,10 +47,10 @@ ADASERVE_HD int32_t row_tiles(int32_t n_nodes, int32_t group, int32_t rows_per_t
 
 // Prefix keys per unit for a request with n_nodes tree nodes.
 ADASERVE_HD int32_t chunk_keys(int32_t n_nodes, int32_t group, int32_t rows_per_tile,
-                               int32_t chunk_target) {
+                               int32_t chunk_target, int32_t floor_mult) {
   const int32_t rows = n_nodes * group < rows_per_tile ? n_nodes * group : rows_per_tile;
   int32_t c = kMinChunk;
-  while (c < 32 * rows && c < kMaxChunk) c *= 2;
+  while (c < floor_mult * rows && c < kMaxChunk) c *= 2;
   return c > chunk_target ? c : chunk_target;
 }
 
@@ -59,20 +59,30 @@ ADASERVE_HD int32_t prefix_chunks(int32_t prefix_len, int32_t chunk) {
 }
 
 ADASERVE_HD int64_t request_units(int32_t n_nodes, int32_t prefix_len, int32_t num_kv_heads,
-                                  int32_t group, int32_t rows_per_tile, int32_t chunk_target) {
+                                  int32_t group, int32_t rows_per_tile, int32_t chunk_target,
+                                  int32_t floor_mult) {
   return (int64_t)num_kv_heads * row_tiles(n_nodes, group, rows_per_tile) *
-         prefix_chunks(prefix_len, chunk_keys(n_nodes, group, rows_per_tile, chunk_target));
+         prefix_chunks(prefix_len, chunk_keys(n_nodes, group, rows_per_tile, chunk_target, floor_mult));
 }
 
 // Workgroup id -> logical unit id.  Hardware deals consecutive workgroup ids
-// to the XCDs round-robin; this sends logical units u, u+1, ... to one XCD so
-// neighbouring units (same KV chunk, different row tiles) share an L2.  The
-// grid must be padded to a multiple of kXcds; ids past `units` do nothing.
+// to the XCDs round-robin.  Logical units are grouped in runs of kXcdRun
+// consecutive ids; run k goes to XCD k % kXcds.  Neighbouring units (the row
+// tiles that read the same KV chunk) therefore share an L2, while every XCD
+// takes its runs from the same moving window of the dispatch order, so the
+// longest-first order is kept chip-wide.  The grid must be padded to a
+// multiple of kXcds * kXcdRun; ids past `units` do nothing.
+constexpr int kXcdRun = 8;
+
 ADASERVE_HD int64_t xcd_swizzle(int64_t block, int64_t padded_grid) {
-  const int64_t per_xcd = padded_grid / kXcds;
-  return (block % kXcds) * per_xcd + block / kXcds;
+  (void)padded_grid;
+  const int64_t x = block % kXcds, j = block / kXcds;
+  return (j / kXcdRun) * (kXcds * kXcdRun) + x * kXcdRun + (j % kXcdRun);
 }
 
-ADASERVE_HD int64_t pad_to_xcds(int64_t n) { return ((n + kXcds - 1) / kXcds) * kXcds; }
+ADASERVE_HD int64_t pad_to_xcds(int64_t n) {
+  const int64_t q = (int64_t)kXcds * kXcdRun;
+  return ((n + q - 1) / q) * q;
+}
 
 }  // namespace adaserve

@@ -77,7 +77,7 @@ __device__ bool locate_request(int64_t idx, bool count_groups, const TreeAttnArg
       n = min(max(n, 0), kMaxTreeNodes);
       const int32_t L = max(a.prefix_len[r], 0);
       ng = (int64_t)a.num_kv_heads * row_tiles(n, a.group, a.rows_per_tile);
-      nu = ng * prefix_chunks(L, chunk_keys(n, a.group, a.rows_per_tile, a.chunk_target));
+      nu = ng * prefix_chunks(L, chunk_keys(n, a.group, a.rows_per_tile, a.chunk_target, a.chunk_floor));
     }
     const int64_t iu = wave_inclusive_scan(nu);
     const int64_t ig = wave_inclusive_scan(ng);
@@ -159,12 +159,20 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
     n = min(max(a.node_indptr[r + 1] - node_base, 0), kMaxTreeNodes);
     L = max(a.prefix_len[r], 0);
   }
+  // Request values are uniform; make that visible so branches on them stay scalar.
+  r = __builtin_amdgcn_readfirstlane(r);
+  node_base = __builtin_amdgcn_readfirstlane(node_base);
+  n = __builtin_amdgcn_readfirstlane(n);
+  L = __builtin_amdgcn_readfirstlane(L);
+  ubase = ((int64_t)__builtin_amdgcn_readfirstlane((int32_t)(ubase >> 32)) << 32) |
+          (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)ubase);
   if (n == 0 || node_base < 0 || node_base + n > a.total_nodes) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = a.group;
   const int RT = a.rows_per_tile;
   const int32_t tiles = row_tiles(n, G, RT);
-  const int32_t chunk_len = chunk_keys(n, G, RT, a.chunk_target);
+  const int32_t chunk_len = chunk_keys(n, G, RT, a.chunk_target, a.chunk_floor);
   const int32_t chunks = prefix_chunks(L, chunk_len);
   const int64_t u = uid - ubase;
   const int32_t tile = (int32_t)(u % tiles);
@@ -218,48 +226,63 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
 
   // ---- DMA addressing: wave-instruction i of this wave fills LDS bytes
   // [(wave*WI + i)*1024, +1024) of a K (or V) stage; lane `lane` lands on key
-  // row dma_row[i], slot dma_slot, so it fetches chunk dma_slot ^ swizzle.
+  // row dma_row[i], slot `slot`, so it fetches chunk slot ^ swizzle(row).
+  // A wave's rows lie in one 16-key page (wave_page of the two in a block),
+  // so the page and its base address are wave-uniform; lanes add a 32-bit
+  // byte offset inside the (page, kv-head) chunk or inside the tree block.
+  const int slot = ((lane * 16) % ROWB) / 16;
+  const int wave_page = (wave * WI * RPI) / kPageSize;
   int dma_row[WI];
-  int64_t dma_col[WI];  // element offset of the chunk inside a key row
+  uint32_t page_off[WI];   // bytes inside the (page, kv-head) chunk
+  uint32_t tree_off[WI];   // bytes from the first key row of the tree block
+  const int64_t tree_stride = (int64_t)a.num_kv_heads * D;   // elements between node rows
 #pragma unroll
   for (int i = 0; i < WI; ++i) {
     dma_row[i] = (wave * WI + i) * RPI + (lane * 16) / ROWB;
-    const int slot = ((lane * 16) % ROWB) / 16;
-    dma_col[i] = (int64_t)((slot ^ swizzle<NCH>(dma_row[i])) * 8);
+    const int chunk_el = (slot ^ swizzle<NCH>(dma_row[i])) * 8;
+    page_off[i] = (uint32_t)(((dma_row[i] % kPageSize) * D + chunk_el) * 2);
+    tree_off[i] = (uint32_t)((dma_row[i] * tree_stride + chunk_el) * 2);
   }
-  const int64_t page_stride = (int64_t)a.num_kv_heads * kPageSize * D;   // elements per page
-  const __bf16 *kpg = (const __bf16 *)a.k_pages + (int64_t)g * kPageSize * D;
-  const __bf16 *vpg = (const __bf16 *)a.v_pages + (int64_t)g * kPageSize * D;
-  const __bf16 *ktr = (const __bf16 *)a.k_tree + ((int64_t)node_base * a.num_kv_heads + g) * D;
-  const __bf16 *vtr = (const __bf16 *)a.v_tree + ((int64_t)node_base * a.num_kv_heads + g) * D;
-  const int64_t tree_stride = (int64_t)a.num_kv_heads * D;
+  const int64_t page_stride_b = (int64_t)a.num_kv_heads * kPageSize * D * 2;   // bytes per page
+  const char *kpg = (const char *)a.k_pages + (int64_t)g * kPageSize * D * 2;
+  const char *vpg = (const char *)a.v_pages + (int64_t)g * kPageSize * D * 2;
+  const char *ktr = (const char *)a.k_tree + ((int64_t)node_base * a.num_kv_heads + g) * D * 2;
+  const char *vtr = (const char *)a.v_tree + ((int64_t)node_base * a.num_kv_heads + g) * D * 2;
   auto issue = [&](char *stage_dst, int blk) {
     char *kdst = stage_dst;
     char *vdst = kdst + BLK;
+    const char *kb, *vb;
+    int rows_left;
+    const bool pre = blk < n_prefix_blocks;
+    if (pre) {
+      const int32_t p = __builtin_amdgcn_readfirstlane(pages[blk * (KB / kPageSize) + wave_page]);
+      rows_left = p >= 0 ? k1 - k0 - blk * KB : 0;
+      kb = kpg + (int64_t)max(p, 0) * page_stride_b;
+      vb = vpg + (int64_t)max(p, 0) * page_stride_b;
+    } else {
+      const int tb = blk - n_prefix_blocks;
+      rows_left = n - tb * KB;
+      kb = ktr + (int64_t)tb * KB * tree_stride * 2;
+      vb = vtr + (int64_t)tb * KB * tree_stride * 2;
+    }
+    if (rows_left >= KB) {
 #pragma unroll
-    for (int i = 0; i < WI; ++i) {
-      const int row = dma_row[i];
-      const void *ks = a.zero16, *vs = a.zero16;
-      if (blk < n_prefix_blocks) {
-        const int32_t t = k0 + blk * KB + row;
-        const int32_t p = pages[blk * (KB / kPageSize) + row / kPageSize];
-        if (t < k1 && p >= 0) {
-          const int64_t off = (int64_t)p * page_stride + (row % kPageSize) * D + dma_col[i];
-          ks = kpg + off;
-          vs = vpg + off;
-        }
-      } else {
-        const int j = (blk - n_prefix_blocks) * KB + row;
-        if (j < n) {
-          const int64_t off = (int64_t)j * tree_stride + dma_col[i];
-          ks = ktr + off;
-          vs = vtr + off;
-        }
+      for (int i = 0; i < WI; ++i) {
+        const uint32_t off = pre ? page_off[i] : tree_off[i];
+        dma16(kb + off, kdst + (wave * WI + i) * 1024);
+        dma16(vb + off, vdst + (wave * WI + i) * 1024);
       }
-      dma16(ks, kdst + (wave * WI + i) * 1024);
-      dma16(vs, vdst + (wave * WI + i) * 1024);
+    } else {
+#pragma unroll
+      for (int i = 0; i < WI; ++i) {
+        const uint32_t off = pre ? page_off[i] : tree_off[i];
+        const bool ok = dma_row[i] < rows_left;
+        dma16(ok ? (const void *)(kb + off) : a.zero16, kdst + (wave * WI + i) * 1024);
+        dma16(ok ? (const void *)(vb + off) : a.zero16, vdst + (wave * WI + i) * 1024);
+      }
     }
   };
+
 
   __syncthreads();  // pages[] and par[] visible
   if (n_blocks > 0) issue(st0, 0);
@@ -308,14 +331,19 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   }
 
   f32x4 o[2][DT];
+  f32x4 osum[2];  // row sums of P, from an all-ones V tile on the matrix cores
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
+  for (int rb = 0; rb < 2; ++rb) {
+    osum[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[rb][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  bf16x8 ones;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
   const float c = a.scale_log2;                      // raw score -> log2 units
   const float up_raw = kRescaleLog2 / c;             // rescale threshold in raw units
   float m_ref[2] = {-1e30f, -1e30f};                 // reference max of this lane's row (raw units)
-  float l_run[2] = {0.f, 0.f};                       // denominator over this lane's keys
 
   // One pipeline step: wait for block blk (at most min(2, n_blocks-1-blk)
   // younger blocks of this wave may still be in flight), barrier (the block
@@ -359,34 +387,30 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
             s[rb][kt][e] = ok ? s[rb][kt][e] : -INFINITY;
           }
       }
-      float bm = fmaxf(fmaxf(fmaxf(s[rb][0][0], s[rb][0][1]), fmaxf(s[rb][0][2], s[rb][0][3])),
-                       fmaxf(fmaxf(s[rb][1][0], s[rb][1][1]), fmaxf(s[rb][1][2], s[rb][1][3])));
+      float bm = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(s[rb][0][0], s[rb][0][1]), s[rb][0][2]),
+                                 __builtin_fmaxf(s[rb][0][3], s[rb][1][0]));
+      bm = __builtin_fmaxf(__builtin_fmaxf(bm, s[rb][1][1]), __builtin_fmaxf(s[rb][1][2], s[rb][1][3]));
       bm = max_over_lane_rows(bm);
       const bool up = bm > m_ref[rb] + up_raw;
       if (__any(up)) {
         const float m_new = up ? bm : m_ref[rb];
         const float alpha = up ? __builtin_amdgcn_exp2f((m_ref[rb] - m_new) * c) : 1.f;
         m_ref[rb] = m_new;
-        l_run[rb] *= alpha;
+        osum[rb] *= alpha;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) o[rb][dt] *= alpha;
       }
       const float mc = m_ref[rb] * c;
-      float psum = 0.f;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[rb][kt][e], c, -mc));
-          s[rb][kt][e] = p;
-          psum += p;
-        }
-      l_run[rb] += psum;
       u32x4 w;
-      w[0] = pack_bf16x2(s[rb][0][0], s[rb][0][1]);
-      w[1] = pack_bf16x2(s[rb][0][2], s[rb][0][3]);
-      w[2] = pack_bf16x2(s[rb][1][0], s[rb][1][1]);
-      w[3] = pack_bf16x2(s[rb][1][2], s[rb][1][3]);
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[rb][kt][0], c, -mc));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[rb][kt][1], c, -mc));
+        const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[rb][kt][2], c, -mc));
+        const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[rb][kt][3], c, -mc));
+        w[kt * 2 + 0] = pack_bf16x2(p0, p1);
+        w[kt * 2 + 1] = pack_bf16x2(p2, p3);
+      }
       pk[rb] = __builtin_bit_cast(bf16x8, w);
     }
 
@@ -395,17 +419,14 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
     // transposed read hands lane (q, j16) V[kbase + e][dt*16 + j16], e < 4.
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(stage + voff[dt]));
-      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(stage + voff[dt] + 16 * ROWB));
-      u32x4 w;
-      w[0] = __builtin_bit_cast(u32x2, lo)[0];
-      w[1] = __builtin_bit_cast(u32x2, lo)[1];
-      w[2] = __builtin_bit_cast(u32x2, hi)[0];
-      w[3] = __builtin_bit_cast(u32x2, hi)[1];
-      const bf16x8 vf = __builtin_bit_cast(bf16x8, w);
+      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(stage + voff[dt]));
+      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(stage + voff[dt] + 16 * ROWB));
+      const bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       o[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pk[0], o[0][dt], 0, 0, 0);
       o[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pk[1], o[1][dt], 0, 0, 0);
     }
+    osum[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pk[0], osum[0], 0, 0, 0);
+    osum[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pk[1], osum[1], 0, 0, 0);
   };
   auto step = [&](const char *cur, char *refill, int blk) {
     const int younger = min(NSTAGE - 2, n_blocks - 1 - blk);
@@ -428,9 +449,7 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   }
 
   const int q4 = q * 4;
-  float l_tot[2];
-#pragma unroll
-  for (int rb = 0; rb < 2; ++rb) l_tot[rb] = sum_over_lane_rows(l_run[rb]);
+  const float l_tot[2] = {osum[0][0], osum[1][0]};
   if (chunks == 1) {
     if (!wave_live) return;
 #pragma unroll
@@ -509,7 +528,7 @@ __global__ __launch_bounds__(kThreads) void tree_attn_combine_kernel(TreeAttnArg
   if (n == 0 || node_base < 0 || node_base + n > a.total_nodes) return;
   const int G = a.group, RT = a.rows_per_tile;
   const int32_t tiles = row_tiles(n, G, RT);
-  const int32_t chunks = prefix_chunks(L, chunk_keys(n, G, RT, a.chunk_target));
+  const int32_t chunks = prefix_chunks(L, chunk_keys(n, G, RT, a.chunk_target, a.chunk_floor));
   if (chunks == 1) return;
   const int64_t u = gid - gbase;
   const int32_t tile = (int32_t)(u % tiles);
