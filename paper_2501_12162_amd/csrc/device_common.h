@@ -32,13 +32,14 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // Max / sum over lanes {l, l^16, l^32, l^48}: the four 16-lane rows of a
 // wave that hold the same MFMA column.  permlane{16,32}_swap exchange rows
 // on the VALU without going through LDS.
+// (NaN-propagating maximum: one v_maximum_f32, no operand canonicalisation.)
 __device__ __forceinline__ float max_over_lane_rows(float v) {
   uint32_t u = __float_as_uint(v);
   auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  float m = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  float m = __builtin_elementwise_maximum(__uint_as_float(a[0]), __uint_as_float(a[1]));
   u = __float_as_uint(m);
   auto b = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+  return __builtin_elementwise_maximum(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
 __device__ __forceinline__ float sum_over_lane_rows(float v) {

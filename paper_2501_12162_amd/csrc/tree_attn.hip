@@ -45,22 +45,51 @@ constexpr int kMaxChunkPages = kMaxChunk / kPageSize;
 // passed in the kernel arguments (resolved once per device on the host).
 __device__ __align__(16) uint32_t g_zero16[4];
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void global_void_t;
+typedef __attribute__((address_space(3))) char lds_char;
 
-// 16 bytes from `src` (per lane) to LDS at `wave_dst` + 16 * lane.
-__device__ __forceinline__ void dma16(const void *src, void *wave_dst) {
-  __builtin_amdgcn_global_load_lds((global_void_t *)src, (lds_void_t *)wave_dst, 16, 0, 0);
+// LDS byte address of a __shared__ object (what M0 takes).
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+  return (uint32_t)(uintptr_t)(const lds_char *)p;
 }
 
-// s_waitcnt encodings (gfx9): vmcnt(N) with the other counters left open,
-// and lgkmcnt(0) with vmcnt left open.
+// 16-byte loads from global memory straight into LDS (global_load_lds):
+// lane l writes LDS bytes [lds + 16 l, +16).  Written as asm so that the
+// compiler does not try to track these loads itself (it cannot follow a
+// ring of stages across the loop and would wait for every load in flight
+// before each LDS read); the "memory" clobber keeps every LDS access in
+// program order around them, and the waits below are counted by hand.
+// Setting M0 needs one wait state before the load that reads it.  The
+// compiler reserves M0 and warns about the clobber; nothing else in this
+// library uses M0 (LDS instructions on gfx950 do not read it).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void *src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(lds) : "memory", "m0");
+}
+// Same with a wave-uniform base address and a 32-bit per-lane offset.
+__device__ __forceinline__ void dma16_off(const void *base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(off), "s"(base), "s"(lds) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// s_waitcnt vmcnt(N) with the other counters left open (for loads the
+// compiler issued itself).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 16, "vmcnt immediate");
   __builtin_amdgcn_s_waitcnt(0xF70 | N);
 }
-__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
+// Waits until at most N of this wave's loads are in flight and its LDS
+// operations are done, then the workgroup barrier.  No memory access moves
+// across it.
+template <int N>
+__device__ __forceinline__ void wait_loads_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt immediate");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(N) : "memory");
+}
 
 // Finds the request that owns logical index `idx`, counting either work units
 // or (kv-head, row tile) groups per request.  Every lane of the wave ends with
@@ -115,18 +144,19 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   constexpr int KS = D / 32;                 // MFMA k-steps over the head dim
   constexpr int DT = D / 16;                 // 16-wide output tiles over the head dim
   constexpr int KB = kKeysPerBlock;          // 32 keys per pipeline stage
-  constexpr int NSTAGE = 4;
   constexpr int ROWB = D * 2;                // bytes per key row
   constexpr int NCH = D / 8;                 // 16-byte chunks per key row
-  constexpr int BLK = KB * ROWB;             // bytes of K (or V) per stage
-  constexpr int WI = BLK / 1024 / 4;         // DMA wave-instructions per wave per tensor
+  constexpr int BLK = KB * ROWB;             // bytes of K (or V) per block
+  constexpr int WI = BLK / 1024 / 4;         // DMA wave-instructions per wave per tensor block
   constexpr int RPI = 1024 / ROWB;           // key rows covered by one wave-instruction
-  constexpr int NDMA = 2 * WI;               // DMA instructions per thread per block
   constexpr float kRescaleLog2 = 8.f;
 
-  // Four pipeline stages, each [K|V][32 keys][D], as separate LDS objects so
-  // the compiler can tell a stage being filled from the stage being read and
-  // does not wait for every in-flight load before each read.
+  // Scores run one block ahead of the PV product: step j multiplies K of
+  // block j+1 and V of block j, and fetches K block j+4 and V block j+3.
+  // Stage t of the four-stage ring holds [K block t+1 | V block t] (mod 4),
+  // so a step reads one stage and refills another.  Every stage is its own
+  // LDS object, so the compiler can tell the stage being filled from the
+  // one being read and does not wait for every load in flight.
   __shared__ __align__(1024) char st0[2 * BLK];
   __shared__ __align__(1024) char st1[2 * BLK];
   __shared__ __align__(1024) char st2[2 * BLK];
@@ -186,8 +216,9 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   const int32_t k0 = chunk * chunk_len;
   const int32_t k1 = min(L, k0 + chunk_len);
   const int32_t n_prefix_blocks = k1 > k0 ? ceil_div(k1 - k0, KB) : 0;
+  const int32_t n_full = k1 > k0 ? (k1 - k0) / KB : 0;   // prefix blocks that need no mask
   const int32_t n_tree_blocks = last_chunk ? ceil_div(n, KB) : 0;
-  const int32_t n_blocks = n_prefix_blocks + n_tree_blocks;
+  const int32_t nb = n_prefix_blocks + n_tree_blocks;
   const int32_t page0 = k0 / kPageSize;
   const int32_t npages = k1 > k0 ? ceil_div(k1, kPageSize) - page0 : 0;
 
@@ -223,13 +254,16 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
       qf[rb][ks] = v;
     }
   }
+  // Let the start-up loads land before the first DMA, so the waits counted
+  // by hand below only ever cover K/V blocks.
+  wait_vmcnt<0>();
 
   // ---- DMA addressing: wave-instruction i of this wave fills LDS bytes
-  // [(wave*WI + i)*1024, +1024) of a K (or V) stage; lane `lane` lands on key
-  // row dma_row[i], slot `slot`, so it fetches chunk slot ^ swizzle(row).
-  // A wave's rows lie in one 16-key page (wave_page of the two in a block),
-  // so the page and its base address are wave-uniform; lanes add a 32-bit
-  // byte offset inside the (page, kv-head) chunk or inside the tree block.
+  // [(wave*WI + i)*1024, +1024) of a stage; lane `lane` lands on key row
+  // dma_row[i], slot `slot`, so it fetches chunk slot ^ swizzle(row).  A
+  // wave's rows lie in one 16-key page (wave_page of the two in a block), so
+  // the page and its base address are wave-uniform; lanes add a 32-bit byte
+  // offset inside the (page, kv-head) chunk or inside the tree block.
   const int slot = ((lane * 16) % ROWB) / 16;
   const int wave_page = (wave * WI * RPI) / kPageSize;
   int dma_row[WI];
@@ -244,50 +278,55 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
     tree_off[i] = (uint32_t)((dma_row[i] * tree_stride + chunk_el) * 2);
   }
   const int64_t page_stride_b = (int64_t)a.num_kv_heads * kPageSize * D * 2;   // bytes per page
-  const char *kpg = (const char *)a.k_pages + (int64_t)g * kPageSize * D * 2;
-  const char *vpg = (const char *)a.v_pages + (int64_t)g * kPageSize * D * 2;
-  const char *ktr = (const char *)a.k_tree + ((int64_t)node_base * a.num_kv_heads + g) * D * 2;
-  const char *vtr = (const char *)a.v_tree + ((int64_t)node_base * a.num_kv_heads + g) * D * 2;
-  auto issue = [&](char *stage_dst, int blk) {
-    char *kdst = stage_dst;
-    char *vdst = kdst + BLK;
-    const char *kb, *vb;
+  const int64_t head_off_b = (int64_t)g * kPageSize * D * 2;
+  const int64_t tree_off_b = ((int64_t)node_base * a.num_kv_heads + g) * D * 2;
+  // Fetches block blk of K (pool = k_pages, tree = k_tree) or of V into
+  // `dst`.  Rows past the end of the block's keys, pages outside the pool and
+  // blocks past the last one come from the zero line: every step issues the
+  // same number of loads, so the waits below are constants.
+  auto issue = [&](const void *pool, const void *tree, char *dst, int blk) {
+    const char *base;
     int rows_left;
     const bool pre = blk < n_prefix_blocks;
-    if (pre) {
+    if (blk >= nb) {
+      rows_left = 0;
+      base = (const char *)tree;
+    } else if (pre) {
       const int32_t p = __builtin_amdgcn_readfirstlane(pages[blk * (KB / kPageSize) + wave_page]);
       rows_left = p >= 0 ? k1 - k0 - blk * KB : 0;
-      kb = kpg + (int64_t)max(p, 0) * page_stride_b;
-      vb = vpg + (int64_t)max(p, 0) * page_stride_b;
+      base = (const char *)pool + head_off_b + (int64_t)max(p, 0) * page_stride_b;
     } else {
       const int tb = blk - n_prefix_blocks;
       rows_left = n - tb * KB;
-      kb = ktr + (int64_t)tb * KB * tree_stride * 2;
-      vb = vtr + (int64_t)tb * KB * tree_stride * 2;
+      base = (const char *)tree + tree_off_b + (int64_t)tb * KB * tree_stride * 2;
     }
+    const uint32_t lds = lds_addr(dst) + wave * WI * 1024;
     if (rows_left >= KB) {
 #pragma unroll
-      for (int i = 0; i < WI; ++i) {
-        const uint32_t off = pre ? page_off[i] : tree_off[i];
-        dma16(kb + off, kdst + (wave * WI + i) * 1024);
-        dma16(vb + off, vdst + (wave * WI + i) * 1024);
-      }
+      for (int i = 0; i < WI; ++i) dma16_off(base, pre ? page_off[i] : tree_off[i], lds + i * 1024);
     } else {
 #pragma unroll
       for (int i = 0; i < WI; ++i) {
-        const uint32_t off = pre ? page_off[i] : tree_off[i];
         const bool ok = dma_row[i] < rows_left;
-        dma16(ok ? (const void *)(kb + off) : a.zero16, kdst + (wave * WI + i) * 1024);
-        dma16(ok ? (const void *)(vb + off) : a.zero16, vdst + (wave * WI + i) * 1024);
+        dma16(ok ? (const void *)(base + (pre ? page_off[i] : tree_off[i])) : a.zero16, lds + i * 1024);
       }
     }
   };
-
+  auto issue_k = [&](char *stage, int blk) { issue(a.k_pages, a.k_tree, stage, blk); };
+  auto issue_v = [&](char *stage, int blk) { issue(a.v_pages, a.v_tree, stage + BLK, blk); };
 
   __syncthreads();  // pages[] and par[] visible
-  if (n_blocks > 0) issue(st0, 0);
-  if (n_blocks > 1) issue(st1, 1);
-  if (n_blocks > 2) issue(st2, 2);
+  // Prologue issue order: K0 (stage 3), then (K1, V0), (K2, V1), (K3, V2)
+  // into stages 0, 1, 2.
+  if (nb > 0) {
+    issue_k(st3, 0);
+    issue_k(st0, 1);
+    issue_v(st0, 0);
+    issue_k(st1, 2);
+    issue_v(st1, 1);
+    issue_k(st2, 3);
+    issue_v(st2, 2);
+  }
 
   // Ancestor sets (while the first blocks are in flight): bit j of node i's
   // set is 1 when j is on i's root-to-node path, i included.  The walk stops
@@ -327,7 +366,7 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
     const int sw = swizzle<NCH>(vrow);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
-      voff[dt] = BLK + vrow * ROWB + (((dt * 2 + ((j16 & 3) >> 1)) ^ sw) * 16) + (j16 & 1) * 8;
+      voff[dt] = vrow * ROWB + (((dt * 2 + ((j16 & 3) >> 1)) ^ sw) * 16) + (j16 & 1) * 8;
   }
 
   f32x4 o[2][DT];
@@ -345,34 +384,29 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   const float up_raw = kRescaleLog2 / c;             // rescale threshold in raw units
   float m_ref[2] = {-1e30f, -1e30f};                 // reference max of this lane's row (raw units)
 
-  // One pipeline step: wait for block blk (at most min(2, n_blocks-1-blk)
-  // younger blocks of this wave may still be in flight), barrier (the block
-  // is complete in LDS and every wave has finished reading the stage that
-  // block blk+3 will fill), issue block blk+3, multiply block blk.
-  auto compute = [&](const char *stage, int blk) {
-    const bool tree_blk = blk >= n_prefix_blocks;
-    const int tb = blk - n_prefix_blocks;
-    const int valid = tree_blk ? min(KB, n - tb * KB) : min(KB, k1 - k0 - blk * KB);
-    const bool need_mask = tree_blk || valid < KB;
-
-    // S^T tiles: s[rb][kt] holds keys kt*16 + q*4 + e of row j16.
-    f32x4 s[2][2];
+  // S^T tiles of one block: s[rb][kt] holds keys kt*16 + q*4 + e of row j16.
+  auto scores = [&](const char *kst, f32x4 (&s)[2][2]) {
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       s[0][kt] = f32x4{0.f, 0.f, 0.f, 0.f};
       s[1][kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 kf = *(const bf16x8 *)(stage + koff[ks] + kt * 16 * ROWB);
+        const bf16x8 kf = *(const bf16x8 *)(kst + koff[ks] + kt * 16 * ROWB);
         s[0][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[0][ks], s[0][kt], 0, 0, 0);
         s[1][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[1][ks], s[1][kt], 0, 0, 0);
       }
     }
-
-    bf16x8 pk[2];
+  };
+  // Masks the partial prefix block and the tree blocks (ancestor sets), then
+  // takes each row's block max.
+  auto mask_max = [&](f32x4 (&s)[2][2], int blk, float (&bm)[2]) {
+    if (blk >= n_full) {
+      const bool tree_blk = blk >= n_prefix_blocks;
+      const int tb = blk - n_prefix_blocks;
+      const int valid = tree_blk ? min(KB, n - tb * KB) : min(KB, k1 - k0 - blk * KB);
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-      if (need_mask) {
+      for (int rb = 0; rb < 2; ++rb) {
         uint32_t aw = 0xffffffffu;
         if (tree_blk) {
           const int node = min((wrow0 + rb * 16 + j16) / G, n - 1);
@@ -387,19 +421,43 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
             s[rb][kt][e] = ok ? s[rb][kt][e] : -INFINITY;
           }
       }
-      float bm = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(s[rb][0][0], s[rb][0][1]), s[rb][0][2]),
-                                 __builtin_fmaxf(s[rb][0][3], s[rb][1][0]));
-      bm = __builtin_fmaxf(__builtin_fmaxf(bm, s[rb][1][1]), __builtin_fmaxf(s[rb][1][2], s[rb][1][3]));
-      bm = max_over_lane_rows(bm);
-      const bool up = bm > m_ref[rb] + up_raw;
-      if (__any(up)) {
-        const float m_new = up ? bm : m_ref[rb];
-        const float alpha = up ? __builtin_amdgcn_exp2f((m_ref[rb] - m_new) * c) : 1.f;
-        m_ref[rb] = m_new;
-        osum[rb] *= alpha;
+    }
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[rb][dt] *= alpha;
+    for (int rb = 0; rb < 2; ++rb) {
+      float m = __builtin_elementwise_maximum(
+          __builtin_elementwise_maximum(s[rb][0][0], s[rb][0][1]), s[rb][0][2]);
+      m = __builtin_elementwise_maximum(__builtin_elementwise_maximum(m, s[rb][0][3]), s[rb][1][0]);
+      m = __builtin_elementwise_maximum(__builtin_elementwise_maximum(m, s[rb][1][1]),
+                                        __builtin_elementwise_maximum(s[rb][1][2], s[rb][1][3]));
+      bm[rb] = max_over_lane_rows(m);
+    }
+  };
+  // Raises the reference max of the rows whose block max went more than
+  // 2^8 above it, rescaling their running numerator and denominator.
+  auto rescale = [&](const float (&bm)[2]) {
+    const bool up0 = bm[0] > m_ref[0] + up_raw;
+    const bool up1 = bm[1] > m_ref[1] + up_raw;
+    if (__any(up0 || up1)) {
+      const float n0 = up0 ? bm[0] : m_ref[0];
+      const float n1 = up1 ? bm[1] : m_ref[1];
+      const float a0 = up0 ? __builtin_amdgcn_exp2f((m_ref[0] - n0) * c) : 1.f;
+      const float a1 = up1 ? __builtin_amdgcn_exp2f((m_ref[1] - n1) * c) : 1.f;
+      m_ref[0] = n0;
+      m_ref[1] = n1;
+      osum[0] *= a0;
+      osum[1] *= a1;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        o[0][dt] *= a0;
+        o[1][dt] *= a1;
       }
+    }
+  };
+  // P = 2^(s c - m c) in bf16, packed as the B operand of the PV product:
+  // k-slot (q, e) is key q*4 + e (e < 4) or 16 + q*4 + (e - 4).
+  auto probs = [&](const f32x4 (&s)[2][2], bf16x8 (&pk)[2]) {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
       const float mc = m_ref[rb] * c;
       u32x4 w;
 #pragma unroll
@@ -413,14 +471,14 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
       }
       pk[rb] = __builtin_bit_cast(bf16x8, w);
     }
-
-    // O^T += V^T P^T.  k-slot (q, e) of the A operand is key q*4 + e (e < 4)
-    // or 16 + q*4 + (e - 4): the keys the packed P fragment carries.  The
-    // transposed read hands lane (q, j16) V[kbase + e][dt*16 + j16], e < 4.
+  };
+  // O^T += V^T P^T and the row sums.  The transposed read hands lane
+  // (q, j16) V[kbase + e][dt*16 + j16], e < 4.
+  auto pv = [&](const char *vst, const bf16x8 (&pk)[2]) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(stage + voff[dt]));
-      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(stage + voff[dt] + 16 * ROWB));
+      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vst + voff[dt]));
+      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vst + voff[dt] + 16 * ROWB));
       const bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       o[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pk[0], o[0][dt], 0, 0, 0);
       o[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pk[1], o[1][dt], 0, 0, 0);
@@ -428,25 +486,71 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
     osum[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pk[0], osum[0], 0, 0, 0);
     osum[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pk[1], osum[1], 0, 0, 0);
   };
-  auto step = [&](const char *cur, char *refill, int blk) {
-    const int younger = min(NSTAGE - 2, n_blocks - 1 - blk);
-    if (younger >= 2) wait_vmcnt<2 * NDMA>();
-    else if (younger == 1) wait_vmcnt<NDMA>();
-    else wait_vmcnt<0>();
-    wait_lgkmcnt0();
-    __builtin_amdgcn_s_barrier();
-    if (blk + NSTAGE - 1 < n_blocks) issue(refill, blk + NSTAGE - 1);
-    if (wave_live) compute(cur, blk);
-  };
-  for (int blk = 0; blk < n_blocks; blk += NSTAGE) {
-    step(st0, st3, blk);
-    if (blk + 1 >= n_blocks) break;
-    step(st1, st0, blk + 1);
-    if (blk + 2 >= n_blocks) break;
-    step(st2, st1, blk + 2);
-    if (blk + 3 >= n_blocks) break;
-    step(st3, st2, blk + 3);
+
+  f32x4 s[2][2];   // scores of the block whose PV product comes next
+  float bm[2];     // their row maxima
+  // Prologue: wait for the whole prologue ring (the loads were issued
+  // together, so K0 alone would land barely earlier; starting the loop with
+  // nothing in flight also keeps the compiler's own wait tracking exact),
+  // then the scores of block 0.  The barrier also publishes the ancestor sets.
+  if (nb > 0) {
+    wait_loads_barrier<0>();
+    if (wave_live) {
+      scores(st3, s);
+      mask_max(s, 0, bm);
+    }
   }
+
+  // Step j: wait until K block j+1 and V block j have landed (the loads of
+  // the two following steps may still fly), barrier (every wave is done with
+  // K block j and V block j-1, whose stages are refilled now), fetch K block
+  // j+4 and V block j+3, then P of block j, scores of block j+1 and the PV
+  // product of block j.  The scores of block j+1 are masked and reduced last,
+  // while the PV products are still running on the matrix cores.
+  auto step = [&](int j, const char *cur, char *fill, bool has_next) {
+    if (has_next) {
+      wait_loads_barrier<4 * WI>();
+      issue_k(fill, j + 4);
+      issue_v(fill, j + 3);
+    } else {
+      wait_loads_barrier<0>();  // also drains the zero-line loads past the last block
+    }
+    if (wave_live) {
+      rescale(bm);
+      bf16x8 pk[2];
+      probs(s, pk);
+      if (has_next) {
+        f32x4 sn[2][2];
+        scores(cur, sn);
+        pv(cur + BLK, pk);
+        mask_max(sn, j + 1, bm);
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) {
+          s[rb][0] = sn[rb][0];
+          s[rb][1] = sn[rb][1];
+        }
+      } else {
+        pv(cur + BLK, pk);
+      }
+    }
+  };
+  int j = 0;
+  for (; j + 1 < nb; j += 4) {
+    step(j, st0, st3, true);
+    if (j + 2 >= nb) { j += 1; break; }
+    step(j + 1, st1, st0, true);
+    if (j + 3 >= nb) { j += 2; break; }
+    step(j + 2, st2, st1, true);
+    if (j + 4 >= nb) { j += 3; break; }
+    step(j + 3, st3, st2, true);
+  }
+  // Last block: nothing is left in flight, so the stage is picked at run time.
+  if (nb > 0) {
+    const int t = (nb - 1) & 3;
+    const char *last = t == 0 ? st0 : t == 1 ? st1 : t == 2 ? st2 : st3;
+    step(nb - 1, last, nullptr, false);
+  }
+  (void)j;
 
   const int q4 = q * 4;
   const float l_tot[2] = {osum[0][0], osum[1][0]};
