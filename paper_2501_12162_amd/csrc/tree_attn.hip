@@ -284,7 +284,12 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   // `dst`.  Rows past the end of the block's keys, pages outside the pool and
   // blocks past the last one come from the zero line: every step issues the
   // same number of loads, so the waits below are constants.
-  auto issue = [&](const void *pool, const void *tree, char *dst, int blk) {
+  // `page` is this wave's physical page of block blk (page_of(blk), read
+  // one step early so the LDS latency stays off the issue path).
+  auto page_of = [&](int blk) -> int32_t {
+    return blk < n_prefix_blocks ? pages[blk * (KB / kPageSize) + wave_page] : -1;
+  };
+  auto issue = [&](const void *pool, const void *tree, char *dst, int blk, int32_t page) {
     const char *base;
     int rows_left;
     const bool pre = blk < n_prefix_blocks;
@@ -292,7 +297,7 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
       rows_left = 0;
       base = (const char *)tree;
     } else if (pre) {
-      const int32_t p = __builtin_amdgcn_readfirstlane(pages[blk * (KB / kPageSize) + wave_page]);
+      const int32_t p = __builtin_amdgcn_readfirstlane(page);
       rows_left = p >= 0 ? k1 - k0 - blk * KB : 0;
       base = (const char *)pool + head_off_b + (int64_t)max(p, 0) * page_stride_b;
     } else {
@@ -312,20 +317,26 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
       }
     }
   };
-  auto issue_k = [&](char *stage, int blk) { issue(a.k_pages, a.k_tree, stage, blk); };
-  auto issue_v = [&](char *stage, int blk) { issue(a.v_pages, a.v_tree, stage + BLK, blk); };
+  auto issue_k = [&](char *stage, int blk, int32_t page) { issue(a.k_pages, a.k_tree, stage, blk, page); };
+  auto issue_v = [&](char *stage, int blk, int32_t page) {
+    issue(a.v_pages, a.v_tree, stage + BLK, blk, page);
+  };
 
   __syncthreads();  // pages[] and par[] visible
   // Prologue issue order: K0 (stage 3), then (K1, V0), (K2, V1), (K3, V2)
   // into stages 0, 1, 2.
+  int32_t pg3 = -1, pg4 = -1;   // pages of blocks j+3 and j+4 at step j
   if (nb > 0) {
-    issue_k(st3, 0);
-    issue_k(st0, 1);
-    issue_v(st0, 0);
-    issue_k(st1, 2);
-    issue_v(st1, 1);
-    issue_k(st2, 3);
-    issue_v(st2, 2);
+    const int32_t pg0 = page_of(0), pg1 = page_of(1), pg2 = page_of(2);
+    pg3 = page_of(3);
+    pg4 = page_of(4);
+    issue_k(st3, 0, pg0);
+    issue_k(st0, 1, pg1);
+    issue_v(st0, 0, pg0);
+    issue_k(st1, 2, pg2);
+    issue_v(st1, 1, pg1);
+    issue_k(st2, 3, pg3);
+    issue_v(st2, 2, pg2);
   }
 
   // Ancestor sets (while the first blocks are in flight): bit j of node i's
@@ -510,8 +521,10 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   auto step = [&](int j, const char *cur, char *fill, bool has_next) {
     if (has_next) {
       wait_loads_barrier<4 * WI>();
-      issue_k(fill, j + 4);
-      issue_v(fill, j + 3);
+      issue_k(fill, j + 4, pg4);
+      issue_v(fill, j + 3, pg3);
+      pg3 = pg4;
+      pg4 = page_of(j + 5);
     } else {
       wait_loads_barrier<0>();  // also drains the zero-line loads past the last block
     }
