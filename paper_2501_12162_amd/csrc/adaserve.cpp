@@ -10,8 +10,11 @@
 #include <cstdio>
 #include <cstring>
 #include <algorithm>
+#include <iterator>
 #include <mutex>
 #include <string>
+#include <utility>
+#include <vector>
 
 #include "kernels.h"
 #include "plan.h"
@@ -118,54 +121,118 @@ struct AttnPlan {
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Throughput figures the planner's cost model uses, measured on MI355X:
-// paged K/V streaming over the whole chip, one workgroup's streaming rate
-// with three 16 KB blocks in flight, the attention loop's compute time per
-// 32-key block of a full 128-row tile (two workgroups sharing a CU), and
-// the gap a second (combine) kernel adds.
-constexpr double kChipBytesPerUs = 6.0e6;
-constexpr double kWgBytesPerUs = 1.9e4;
-constexpr double kBlockComputeUs = 1.14;
-constexpr double kCombineGapUs = 3.0;
+// Cost model of the bf16 kernel, measured on MI355X: paged K/V streaming
+// over the whole chip; one 32-key pipeline step of a workgroup while two
+// workgroups share each CU (it hardly depends on the tile's row count: the
+// four waves compute their row blocks side by side); the fixed cost of a
+// unit (first loads of the block table, queries and K block 0, then the
+// output writes); and the latency the combine kernel adds.
+constexpr double kChipBytesPerUs = 5.8e6;
+constexpr double kBlockUs = 1.0;
+constexpr double kUnitFixedUs = 6.0;
+constexpr double kCombineUs = 3.0;
 constexpr int kCUs = 256;
+constexpr int kSlots = 2 * kCUs;  // resident workgroups: two per CU
 
-// Plan for one (row tile, chunk target, chunk floor) choice, with its cost
-// estimate: the larger of the chip-wide streaming time and the longest unit
-// (whose stream and compute overlap), plus the combine pass when a prefix
-// is split.
+// Makespan of units dispatched longest first onto kSlots workgroup slots,
+// each unit taking the slot that frees up first (how the hardware deals a
+// grid whose units come in that order).  Slot loads are kept as runs of
+// equal load, so the cost grows with the number of distinct durations, not
+// with the number of units.  `units` holds (duration, count) pairs in any
+// order; it is sorted in place.
+double lpt_makespan(std::vector<std::pair<double, int64_t>> &units) {
+  std::sort(units.begin(), units.end(), [](const auto &x, const auto &y) { return x.first > y.first; });
+  size_t m = 0;  // merge equal durations
+  for (size_t i = 0; i < units.size(); ++i) {
+    if (m > 0 && units[m - 1].first == units[i].first)
+      units[m - 1].second += units[i].second;
+    else
+      units[m++] = units[i];
+  }
+  units.resize(m);
+  std::vector<std::pair<double, int64_t>> runs{{0.0, (int64_t)kSlots}};  // (load, slots), ascending
+  std::vector<std::pair<double, int64_t>> moved, rest, merged;
+  for (const auto &u : units) {
+    const double t = u.first;
+    int64_t c = u.second;
+    const int64_t rounds = c / kSlots;
+    if (rounds > 0) {
+      for (auto &x : runs) x.first += (double)rounds * t;
+      c -= rounds * kSlots;
+    }
+    if (c == 0) continue;
+    // the c least-loaded slots take one more unit each: an ascending prefix
+    // of the runs moves up by t, so two ascending lists are merged back
+    moved.clear();
+    rest.clear();
+    for (const auto &x : runs) {
+      if (c == 0) {
+        rest.push_back(x);
+      } else if (x.second <= c) {
+        moved.push_back({x.first + t, x.second});
+        c -= x.second;
+      } else {
+        moved.push_back({x.first + t, c});
+        rest.push_back({x.first, x.second - c});
+        c = 0;
+      }
+    }
+    merged.clear();
+    std::merge(rest.begin(), rest.end(), moved.begin(), moved.end(), std::back_inserter(merged));
+    runs.clear();
+    for (const auto &x : merged) {
+      if (!runs.empty() && runs.back().first == x.first)
+        runs.back().second += x.second;
+      else
+        runs.push_back(x);
+    }
+  }
+  return runs.back().first;
+}
+
+// Plan for one (chunk target, chunk floor) choice with 128-row tiles.  The
+// cost estimate is the larger of the longest-first makespan of the units
+// and the chip-wide streaming time (K/V plus the split partials), plus the
+// combine pass when a prefix is split.  evaluate_plan fills everything but
+// the makespan and returns the unit list; `bound` is a lower bound of the
+// estimate (the makespan replaced by max(longest unit, total / slots)).
 AttnPlan evaluate_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
                        int32_t group, int32_t head_dim, int32_t rows_per_tile, int32_t chunk_target,
-                       int32_t floor_mult) {
+                       int32_t floor_mult, std::vector<std::pair<double, int64_t>> &units, double &fixed,
+                       double &bound) {
   AttnPlan p;
   p.rows_per_tile = rows_per_tile;
   p.chunk_target = chunk_target;
   p.chunk_floor = floor_mult;
   const double key_bytes = 4.0 * head_dim;  // bf16 K and V of one key of one kv-head
-  double kv_bytes = 0, partial_bytes = 0, longest = 0, work = 0;
+  double kv_bytes = 0, partial_bytes = 0, total = 0;
+  units.clear();
   for (int32_t r = 0; r < B; ++r) {
     const int32_t n = indptr_host[r + 1] - indptr_host[r];
     const int32_t L = plen_host[r];
     const int32_t tiles = row_tiles(n, group, rows_per_tile);
     const int32_t ck = chunk_keys(n, group, rows_per_tile, chunk_target, floor_mult);
     const int32_t chunks = prefix_chunks(L, ck);
-    p.units += (int64_t)hkv * tiles * chunks;
+    const int64_t cnt = (int64_t)hkv * tiles * chunks;
+    p.units += cnt;
     p.row_groups += (int64_t)hkv * tiles;
-    kv_bytes += (double)hkv * (L + n) * key_bytes;
+    kv_bytes += (double)hkv * tiles * (L + n) * key_bytes;
     if (chunks > 1) {
       p.needs_combine = true;
-      partial_bytes += (double)hkv * chunks * n * group * (head_dim + 2) * 4.0;
+      partial_bytes += hkv * chunks * n * group * (head_dim + 2) * 4.0;
     }
-    const int32_t rows = std::min(n * group, rows_per_tile);
-    const double keys = std::min(L, ck) + n;
-    const double blocks = keys / 32.0;
-    const double t_unit = std::max(keys * key_bytes / kWgBytesPerUs,
-                                   blocks * kBlockComputeUs * std::max(rows, 32) / 128.0);
-    longest = std::max(longest, t_unit);
-    work += (double)hkv * tiles * chunks * t_unit;
+    // every chunk pays the fixed cost; the tree block is spread over them
+    const double blocks = ceil_div(std::min(L, ck), 32) + (double)ceil_div(n, 32) / chunks;
+    units.push_back({kUnitFixedUs + blocks * kBlockUs, cnt});
+    total += units.back().first * cnt;
   }
-  const double slots = 2.0 * kCUs;
-  const double t_main = std::max({(kv_bytes + partial_bytes) / kChipBytesPerUs, longest, work / slots});
-  p.est_us = t_main + (p.needs_combine ? kCombineGapUs + 2.0 * partial_bytes / kChipBytesPerUs : 0.0);
+  double longest = 0;
+  for (const auto &u : units) longest = std::max(longest, u.first);
+  const double stream = (kv_bytes + partial_bytes) / kChipBytesPerUs;
+  const double combine = p.needs_combine ? kCombineUs + partial_bytes / kChipBytesPerUs : 0.0;
+  fixed = combine;
+  p.est_us = std::max(stream, 0.0);  // completed with the makespan by make_plan
+  bound = std::max({stream, longest, total / kSlots}) + combine;
   p.padded_grid = pad_to_xcds(p.units);
   if (p.needs_combine) {
     p.ws_o_bytes = round_up((size_t)p.units * kMaxRowsPerTile * head_dim * sizeof(float), 256);
@@ -176,23 +243,52 @@ AttnPlan evaluate_plan(int32_t B, const int32_t *indptr_host, const int32_t *ple
 }
 
 // Work plan of the bf16 kernel, from host-visible sizes only: the cheapest
-// estimate over row tiles {64, 128}, chunk targets {256 .. 8192} and chunk
-// floors {8, 16, 32} keys per row (see evaluate_plan).  Requests are then
-// dispatched in descending order of per-unit cost (fill_plan_table).
+// estimate over chunk targets {256 .. 8192} and chunk floors {8, 16, 32}
+// keys per row (see evaluate_plan), 128-row tiles.  (A 64-row tile makes
+// two units read the same K/V for about the same step time, so it never
+// wins.)  Choices that give every request the same chunk length as one
+// already tried are skipped, and the makespan is only simulated for
+// choices whose lower bound can still beat the best estimate so far.
+// Requests are then dispatched in descending order of per-unit cost
+// (fill_plan_table).
 AttnPlan make_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
                    int32_t group, int32_t head_dim, int32_t dtype) {
   AttnPlan best;
   if (dtype != ADASERVE_BF16 || B == 0) return best;
-  bool have = false;
-  for (int32_t rt : {128, 64})
-    for (int32_t fm : {32, 16, 8})
-      for (int32_t c = kMaxChunk; c >= kMinChunk; c /= 2) {
-        AttnPlan p = evaluate_plan(B, indptr_host, plen_host, hkv, group, head_dim, rt, c, fm);
-        if (!have || p.est_us < best.est_us * 0.98) {
-          best = p;
-          have = true;
-        }
+  const int32_t rt = kMaxRowsPerTile;
+  struct Cand {
+    double bound;
+    int32_t fm, c;
+  };
+  std::vector<Cand> cands;
+  std::vector<std::vector<int32_t>> seen;
+  std::vector<int32_t> cks(B);
+  std::vector<std::pair<double, int64_t>> units;
+  double fixed, bound;
+  for (int32_t fm : {32, 16, 8})
+    for (int32_t c = kMaxChunk; c >= kMinChunk; c /= 2) {
+      for (int32_t r = 0; r < B; ++r) {
+        const int32_t n = indptr_host[r + 1] - indptr_host[r];
+        const int32_t ck = chunk_keys(n, group, rt, c, fm);
+        cks[r] = prefix_chunks(plen_host[r], ck) > 1 ? ck : 0;  // 0: unsplit
       }
+      if (std::find(seen.begin(), seen.end(), cks) != seen.end()) continue;
+      seen.push_back(cks);
+      evaluate_plan(B, indptr_host, plen_host, hkv, group, head_dim, rt, c, fm, units, fixed, bound);
+      cands.push_back({bound, fm, c});
+    }
+  // candidates in the order they were generated break ties (larger chunks first)
+  std::stable_sort(cands.begin(), cands.end(), [](const Cand &x, const Cand &y) { return x.bound < y.bound; });
+  bool have = false;
+  for (const Cand &cd : cands) {
+    if (have && cd.bound >= best.est_us * 0.98) break;
+    AttnPlan p = evaluate_plan(B, indptr_host, plen_host, hkv, group, head_dim, rt, cd.c, cd.fm, units, fixed, bound);
+    p.est_us = std::max(p.est_us, lpt_makespan(units)) + fixed;
+    if (!have || p.est_us < best.est_us * 0.98) {
+      best = p;
+      have = true;
+    }
+  }
   return best;
 }
 
@@ -206,10 +302,9 @@ void fill_plan_table(TreeAttnArgs &a, int32_t B, const int32_t *indptr_host, con
   int64_t cost[kPlanMax];
   for (int32_t r = 0; r < B; ++r) {
     const int32_t n = indptr_host[r + 1] - indptr_host[r];
-    const int32_t rows = std::min(n * a.group, p.rows_per_tile);
     const int32_t keys = std::min(std::max(plen_host[r], 0),
                                   chunk_keys(n, a.group, p.rows_per_tile, p.chunk_target, p.chunk_floor));
-    cost[r] = (int64_t)(keys + n) * rows;
+    cost[r] = keys + n;  // steps per unit (the step time hardly depends on the row count)
     order[r] = r;
   }
   std::stable_sort(order, order + B, [&](int32_t x, int32_t y) { return cost[x] > cost[y]; });

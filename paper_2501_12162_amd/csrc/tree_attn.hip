@@ -500,12 +500,10 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
 
   f32x4 s[2][2];   // scores of the block whose PV product comes next
   float bm[2];     // their row maxima
-  // Prologue: wait for the whole prologue ring (the loads were issued
-  // together, so K0 alone would land barely earlier; starting the loop with
-  // nothing in flight also keeps the compiler's own wait tracking exact),
-  // then the scores of block 0.  The barrier also publishes the ancestor sets.
+  // Prologue: wait for K0 (the six later prologue loads may still fly), then
+  // the scores of block 0.  The barrier also publishes the ancestor sets.
   if (nb > 0) {
-    wait_loads_barrier<0>();
+    wait_loads_barrier<6 * WI>();
     if (wave_live) {
       scores(st3, s);
       mask_max(s, 0, bm);
