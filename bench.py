@@ -276,6 +276,14 @@ def main():
             "node_argmax_alg_bytes": costs["argmax_bytes"],
             "tree_accept_us": accept_us,
             "step_event_sum_us": attn_us + argmax_us + accept_us,
+            "path_hbm_frac": (costs["attn_bytes"] + costs["argmax_bytes"])
+            / ((attn_us + argmax_us + accept_us) * 1e-6) / 1e9 / HBM_PEAK_GBS,
+            "percentiles_us": {
+                name: {"p10": float(np.percentile(x, 10)) * 1e3, "p50": float(np.median(x)) * 1e3,
+                       "p90": float(np.percentile(x, 90)) * 1e3}
+                for name, x in (("tree_attn", attn_ms), ("node_argmax", argmax_ms), ("tree_accept", accept_ms),
+                                ("step", attn_ms + argmax_ms + accept_ms))
+            },
         },
         "accepted_tokens_per_step": int(alen.sum()),
         "accepted_tokens_per_s": float(alen.sum()) * args.steps / wall,
