@@ -28,6 +28,7 @@
 //    fully parallel kernel merges them (the kernel boundary makes the
 //    partials of every XCD visible without per-workgroup cache flushes).
 #include <mutex>
+#include <type_traits>
 
 #include "device_common.h"
 #include "kernels.h"
@@ -152,18 +153,19 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   constexpr float kRescaleLog2 = 8.f;
 
   // Scores run one block ahead of the PV product: step j multiplies K of
-  // block j+1 and V of block j, and fetches K block j+4 and V block j+3.
-  // Stage t of the four-stage ring holds [K block t+1 | V block t] (mod 4),
-  // so a step reads one stage and refills another.  Every stage is its own
-  // LDS object, so the compiler can tell the stage being filled from the
-  // one being read and does not wait for every load in flight.
-  __shared__ __align__(1024) char st0[2 * BLK];
-  __shared__ __align__(1024) char st1[2 * BLK];
-  __shared__ __align__(1024) char st2[2 * BLK];
-  __shared__ __align__(1024) char st3[2 * BLK];
-  __shared__ __align__(16) uint32_t anc[kMaxTreeNodes * 4];
-  __shared__ int32_t pages[kMaxChunkPages];
-  __shared__ int32_t par[kMaxTreeNodes];
+  // block j+1 and V of block j, and fetches K block j+5 and V block j+4.
+  // Stage t of the five-stage ring holds [K block t+1 | V block t] (mod 5),
+  // so a step reads one stage and refills another, and four of the five
+  // stages are in flight while one is multiplied.  The ring is all the LDS
+  // this kernel has (80 KB at D = 128, two workgroups per CU): page ids are
+  // read from the block table with scalar loads, and the parents and
+  // ancestor sets live in the V half of stage 4 until the first step
+  // refills it (each lane keeps its own rows' ancestor sets in registers).
+  constexpr int NST = 5;
+  __shared__ __align__(1024) char ring[NST * 2 * BLK];
+  int32_t *const par = (int32_t *)(ring + (NST - 1) * 2 * BLK + BLK);
+  uint32_t *const anc = (uint32_t *)(ring + (NST - 1) * 2 * BLK + BLK + kMaxTreeNodes * 4);
+  static_assert(kMaxTreeNodes * 4 * 5 <= BLK, "parents and ancestor sets fit in a V half-stage");
 
   const int64_t uid = xcd_swizzle(blockIdx.x, a.padded_grid);
   if (uid >= a.units) return;
@@ -222,15 +224,25 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   const int32_t page0 = k0 / kPageSize;
   const int32_t npages = k1 > k0 ? ceil_div(k1, kPageSize) - page0 : 0;
 
-  // ---- start-up: block table, parents and queries, all loads in flight together
-  for (int i = tid; i < npages; i += kThreads) {
+  // ---- start-up: page ids, parents and queries, all loads in flight together.
+  // The DMA rows of a wave lie in one 16-key page of each 32-key block (page
+  // wave_page of the two); lane l of pgv[i] holds that page's id in prefix
+  // block i*64 + l, or -1.
+  const int wave_page = (wave * WI * RPI) / kPageSize;
+  static_assert(kMaxChunk / KB <= 4 * 64, "page ids of a chunk fit in four lanes-wide registers");
+  int32_t pgv[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int32_t blk = i * 64 + lane;
+    const int32_t e = page0 + blk * (KB / kPageSize) + wave_page;
     int32_t p = -1;
-    if (page0 + i < a.bt_stride) {
-      p = a.block_table[(int64_t)r * a.bt_stride + page0 + i];
+    if (blk < n_prefix_blocks && e < a.bt_stride) {
+      p = a.block_table[(int64_t)r * a.bt_stride + e];
       if (p < 0 || p >= a.num_pages) p = -1;
     }
-    pages[i] = p;
+    pgv[i] = p;
   }
+  (void)npages;
   if (last_chunk)
     for (int i = tid; i < n; i += kThreads) par[i] = a.parent[node_base + i];
 
@@ -265,7 +277,6 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   // the page and its base address are wave-uniform; lanes add a 32-bit byte
   // offset inside the (page, kv-head) chunk or inside the tree block.
   const int slot = ((lane * 16) % ROWB) / 16;
-  const int wave_page = (wave * WI * RPI) / kPageSize;
   int dma_row[WI];
   uint32_t page_off[WI];   // bytes inside the (page, kv-head) chunk
   uint32_t tree_off[WI];   // bytes from the first key row of the tree block
@@ -284,10 +295,15 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   // `dst`.  Rows past the end of the block's keys, pages outside the pool and
   // blocks past the last one come from the zero line: every step issues the
   // same number of loads, so the waits below are constants.
-  // `page` is this wave's physical page of block blk (page_of(blk), read
-  // one step early so the LDS latency stays off the issue path).
+  // `page` is this wave's physical page of block blk, or -1 (tree block,
+  // entry past the block table row, or a page id outside the pool), read from
+  // the page-id registers with lane reads (blk is uniform).
   auto page_of = [&](int blk) -> int32_t {
-    return blk < n_prefix_blocks ? pages[blk * (KB / kPageSize) + wave_page] : -1;
+    if (blk >= n_prefix_blocks) return -1;
+    const int l = blk & 63, hi = blk >> 6;
+    const int32_t p0 = __builtin_amdgcn_readlane(pgv[0], l), p1 = __builtin_amdgcn_readlane(pgv[1], l);
+    const int32_t p2 = __builtin_amdgcn_readlane(pgv[2], l), p3 = __builtin_amdgcn_readlane(pgv[3], l);
+    return hi == 0 ? p0 : hi == 1 ? p1 : hi == 2 ? p2 : p3;
   };
   auto issue = [&](const void *pool, const void *tree, char *dst, int blk, int32_t page) {
     const char *base;
@@ -322,21 +338,23 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
     issue(a.v_pages, a.v_tree, stage + BLK, blk, page);
   };
 
-  __syncthreads();  // pages[] and par[] visible
-  // Prologue issue order: K0 (stage 3), then (K1, V0), (K2, V1), (K3, V2)
-  // into stages 0, 1, 2.
-  int32_t pg3 = -1, pg4 = -1;   // pages of blocks j+3 and j+4 at step j
+  __syncthreads();  // par[] visible
+  // Prologue issue order: K0 (stage 4), then (K1, V0), (K2, V1), (K3, V2),
+  // (K4, V3) into stages 0 .. 3.
+  int32_t pg4 = -1, pg5 = -1;   // pages of blocks j+4 and j+5 at step j
   if (nb > 0) {
-    const int32_t pg0 = page_of(0), pg1 = page_of(1), pg2 = page_of(2);
-    pg3 = page_of(3);
+    const int32_t pg0 = page_of(0), pg1 = page_of(1), pg2 = page_of(2), pg3 = page_of(3);
     pg4 = page_of(4);
-    issue_k(st3, 0, pg0);
-    issue_k(st0, 1, pg1);
-    issue_v(st0, 0, pg0);
-    issue_k(st1, 2, pg2);
-    issue_v(st1, 1, pg1);
-    issue_k(st2, 3, pg3);
-    issue_v(st2, 2, pg2);
+    pg5 = page_of(5);
+    issue_k(ring + 4 * 2 * BLK, 0, pg0);
+    issue_k(ring + 0 * 2 * BLK, 1, pg1);
+    issue_v(ring + 0 * 2 * BLK, 0, pg0);
+    issue_k(ring + 1 * 2 * BLK, 2, pg2);
+    issue_v(ring + 1 * 2 * BLK, 1, pg1);
+    issue_k(ring + 2 * 2 * BLK, 3, pg3);
+    issue_v(ring + 2 * 2 * BLK, 2, pg2);
+    issue_k(ring + 3 * 2 * BLK, 4, pg4);
+    issue_v(ring + 3 * 2 * BLK, 3, pg3);
   }
 
   // Ancestor sets (while the first blocks are in flight): bit j of node i's
@@ -368,6 +386,16 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
 
   // Per-lane LDS offsets of the MFMA operand fragments inside a stage.
   const int q = lane >> 4, j16 = lane & 15;
+
+  // The ancestor sets of this lane's two rows' nodes, in registers (named
+  // scalars: an indexed array would be placed in scratch memory).
+  uint32_t an00 = 0, an01 = 0, an02 = 0, an03 = 0, an10 = 0, an11 = 0, an12 = 0, an13 = 0;
+  if (last_chunk) {
+    __syncthreads();  // anc[] complete
+    const int node0 = min((wrow0 + j16) / G, n - 1), node1 = min((wrow0 + 16 + j16) / G, n - 1);
+    an00 = anc[node0 * 4 + 0], an01 = anc[node0 * 4 + 1], an02 = anc[node0 * 4 + 2], an03 = anc[node0 * 4 + 3];
+    an10 = anc[node1 * 4 + 0], an11 = anc[node1 * 4 + 1], an12 = anc[node1 * 4 + 2], an13 = anc[node1 * 4 + 3];
+  }
   int koff[KS];  // K fragment for keys kt*16 + j16 (add kt*16*ROWB), chunk ks*4 + q
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) koff[ks] = j16 * ROWB + (((ks * 4 + q) ^ swizzle<NCH>(j16)) * 16);
@@ -409,10 +437,9 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
       }
     }
   };
-  // Masks the partial prefix block and the tree blocks (ancestor sets), then
-  // takes each row's block max.
-  auto mask_max = [&](f32x4 (&s)[2][2], int blk, float (&bm)[2]) {
-    if (blk >= n_full) {
+  // Masks the partial prefix block and the tree blocks (ancestor sets).
+  auto mask = [&](f32x4 (&s)[2][2], int blk) {
+    {
       const bool tree_blk = blk >= n_prefix_blocks;
       const int tb = blk - n_prefix_blocks;
       const int valid = tree_blk ? min(KB, n - tb * KB) : min(KB, k1 - k0 - blk * KB);
@@ -420,8 +447,9 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
       for (int rb = 0; rb < 2; ++rb) {
         uint32_t aw = 0xffffffffu;
         if (tree_blk) {
-          const int node = min((wrow0 + rb * 16 + j16) / G, n - 1);
-          aw = anc[node * 4 + tb];
+          const uint32_t w0 = rb ? an10 : an00, w1 = rb ? an11 : an01;
+          const uint32_t w2 = rb ? an12 : an02, w3 = rb ? an13 : an03;
+          aw = (tb & 2) ? ((tb & 1) ? w3 : w2) : ((tb & 1) ? w1 : w0);
         }
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
@@ -433,6 +461,9 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
           }
       }
     }
+  };
+  // Each row's block max.
+  auto rowmax = [&](const f32x4 (&s)[2][2], float (&bm)[2]) {
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
       float m = __builtin_elementwise_maximum(
@@ -500,29 +531,35 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
 
   f32x4 s[2][2];   // scores of the block whose PV product comes next
   float bm[2];     // their row maxima
-  // Prologue: wait for K0 (the six later prologue loads may still fly), then
-  // the scores of block 0.  The barrier also publishes the ancestor sets.
+  // Prologue: wait for K0 (the eight later prologue loads may still fly),
+  // then the scores of block 0.
   if (nb > 0) {
-    wait_loads_barrier<6 * WI>();
+    wait_loads_barrier<8 * WI>();
     if (wave_live) {
-      scores(st3, s);
-      mask_max(s, 0, bm);
+      scores(ring + 4 * 2 * BLK, s);
+      if (n_full == 0) mask(s, 0);
+      rowmax(s, bm);
     }
   }
 
-  // Step j: wait until K block j+1 and V block j have landed (the loads of
-  // the two following steps may still fly), barrier (every wave is done with
-  // K block j and V block j-1, whose stages are refilled now), fetch K block
-  // j+4 and V block j+3, then P of block j, scores of block j+1 and the PV
-  // product of block j.  The scores of block j+1 are masked and reduced last,
-  // while the PV products are still running on the matrix cores.
-  auto step = [&](int j, const char *cur, char *fill, bool has_next) {
-    if (has_next) {
-      wait_loads_barrier<4 * WI>();
-      issue_k(fill, j + 4, pg4);
-      issue_v(fill, j + 3, pg3);
-      pg3 = pg4;
-      pg4 = page_of(j + 5);
+  // Step j (its stage is cs = j mod 5): wait until K block j+1 and V block j
+  // have landed (the loads of the three following steps may still fly),
+  // barrier (every wave is done with K block j and V block j-1, whose stage
+  // is refilled now), fetch K block j+5 and V block j+4, then P of block j,
+  // scores of block j+1 and the PV product of block j; the scores of block
+  // j+1 are masked (when they need it) and reduced last, while the PV
+  // products run on the matrix cores.
+  auto step = [&](int j, int cs, auto masked, auto has_next) {
+    constexpr bool kMasked = decltype(masked)::value;
+    constexpr bool kNext = decltype(has_next)::value;
+    const char *cur = ring + cs * (2 * BLK);
+    if constexpr (kNext) {
+      wait_loads_barrier<6 * WI>();
+      char *fill = ring + (cs == 0 ? NST - 1 : cs - 1) * (2 * BLK);
+      issue_k(fill, j + 5, pg5);
+      issue_v(fill, j + 4, pg4);
+      pg4 = pg5;
+      pg5 = page_of(j + 6);
     } else {
       wait_loads_barrier<0>();  // also drains the zero-line loads past the last block
     }
@@ -530,11 +567,12 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
       rescale(bm);
       bf16x8 pk[2];
       probs(s, pk);
-      if (has_next) {
+      if constexpr (kNext) {
         f32x4 sn[2][2];
         scores(cur, sn);
         pv(cur + BLK, pk);
-        mask_max(sn, j + 1, bm);
+        if constexpr (kMasked) mask(sn, j + 1);
+        rowmax(sn, bm);
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb) {
           s[rb][0] = sn[rb][0];
@@ -545,23 +583,13 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
       }
     }
   };
-  int j = 0;
-  for (; j + 1 < nb; j += 4) {
-    step(j, st0, st3, true);
-    if (j + 2 >= nb) { j += 1; break; }
-    step(j + 1, st1, st0, true);
-    if (j + 3 >= nb) { j += 2; break; }
-    step(j + 2, st2, st1, true);
-    if (j + 4 >= nb) { j += 3; break; }
-    step(j + 3, st3, st2, true);
-  }
-  // Last block: nothing is left in flight, so the stage is picked at run time.
-  if (nb > 0) {
-    const int t = (nb - 1) & 3;
-    const char *last = t == 0 ? st0 : t == 1 ? st1 : t == 2 ? st2 : st3;
-    step(nb - 1, last, nullptr, false);
-  }
-  (void)j;
+  using Yes = std::true_type;
+  using No = std::false_type;
+  int j = 0, cs = 0;
+  auto next_stage = [](int c) { return c == NST - 1 ? 0 : c + 1; };
+  for (; j + 1 < n_full; ++j, cs = next_stage(cs)) step(j, cs, No{}, Yes{});  // block j+1: full prefix block
+  for (; j + 1 < nb; ++j, cs = next_stage(cs)) step(j, cs, Yes{}, Yes{});     // block j+1 needs the mask
+  if (nb > 0) step(nb - 1, cs, No{}, No{});
 
   const int q4 = q * 4;
   const float l_tot[2] = {osum[0][0], osum[1][0]};
