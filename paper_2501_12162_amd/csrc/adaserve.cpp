@@ -219,7 +219,7 @@ AttnPlan evaluate_plan(int32_t B, const int32_t *indptr_host, const int32_t *ple
     kv_bytes += (double)hkv * tiles * (L + n) * key_bytes;
     if (chunks > 1) {
       p.needs_combine = true;
-      partial_bytes += hkv * chunks * n * group * (head_dim + 2) * 4.0;
+      partial_bytes += hkv * chunks * n * group * (head_dim * 2.0 + 8.0);
     }
     // every chunk pays the fixed cost; the tree block is spread over them
     const double blocks = ceil_div(std::min(L, ck), 32) + (double)ceil_div(n, 32) / chunks;
@@ -235,7 +235,7 @@ AttnPlan evaluate_plan(int32_t B, const int32_t *indptr_host, const int32_t *ple
   bound = std::max({stream, longest, total / kSlots}) + combine;
   p.padded_grid = pad_to_xcds(p.units);
   if (p.needs_combine) {
-    p.ws_o_bytes = round_up((size_t)p.units * kMaxRowsPerTile * head_dim * sizeof(float), 256);
+    p.ws_o_bytes = round_up((size_t)p.units * kMaxRowsPerTile * head_dim * 2, 256);  // bf16
     p.ws_ml_bytes = round_up((size_t)p.units * kMaxRowsPerTile * 2 * sizeof(float), 256);
     p.ws_bytes = p.ws_o_bytes + p.ws_ml_bytes;
   }
@@ -394,7 +394,7 @@ int32_t adaserve_tree_attn_verify(int32_t num_requests, const int32_t *node_indp
   a.k_pages = k_pages;
   a.v_pages = v_pages;
   a.out = out;
-  a.ws_o = plan.ws_bytes ? (float *)workspace : nullptr;
+  a.ws_o = plan.ws_bytes ? (__bf16 *)workspace : nullptr;
   a.ws_ml = plan.ws_bytes ? (float *)((char *)workspace + plan.ws_o_bytes) : nullptr;
   a.num_requests = num_requests;
   a.total_nodes = shape.total_nodes;

@@ -32,7 +32,7 @@ struct TreeAttnArgs {
   const void *v_pages;
   const void *zero16;          // 16 zero bytes in device memory (source of masked DMA lanes)
   void *out;                   // [T, Hq, D]
-  float *ws_o;                 // [units, kMaxRowsPerTile, D] partial numerators
+  __bf16 *ws_o;                // [units, kMaxRowsPerTile, D] partial outputs (each chunk normalised)
   float *ws_ml;                // [units, kMaxRowsPerTile, 2]  (reference max in raw units, denominator)
   int32_t num_requests;
   int32_t total_nodes;

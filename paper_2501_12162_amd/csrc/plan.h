@@ -15,8 +15,11 @@
 // 16 or 32); above that floor the batch-wide `chunk_target` sets the split.
 //
 // Units are numbered request by request; inside a request the order is
-// (g, chunk, tile) with the tile fastest, so the tiles that read the same KV
-// chunk are neighbours (and mostly land on one XCD, see xcd_swizzle).
+// (chunk, g, tile) with the tile fastest, so the tiles that read the same KV
+// chunk are neighbours (and mostly land on one XCD, see xcd_swizzle), and
+// the neighbouring runs of units that an XCD takes cover every kv-head: a
+// kv-head's (page, head) chunks sit at one offset inside every page, and an
+// XCD that read only one head measured markedly slower than the others.
 //
 // The host planner and the device-side unit lookup both use the functions
 // below, so their arithmetic cannot drift apart.

@@ -92,6 +92,26 @@ __device__ __forceinline__ void wait_loads_barrier() {
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(N) : "memory");
 }
 
+// Index of the first plan entry whose unit_end (or group_end) exceeds `key`,
+// or -1: every lane reads one entry per 64, so the whole table costs one
+// round of loads instead of a chain of dependent ones.  Uniform result.
+__device__ __forceinline__ int find_plan_entry(const TreeAttnArgs &a, int64_t key, bool groups) {
+  static_assert(kPlanMax <= 3 * 64, "three rounds of 64 lanes cover the plan table");
+  const int lane = threadIdx.x & 63;
+  int32_t end[3];
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    const int i = k * 64 + lane;
+    end[k] = i < a.plan_count ? (groups ? a.plan[i].group_end : a.plan[i].unit_end) : INT32_MAX;
+  }
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    const unsigned long long hit = __ballot((int64_t)end[k] > key);
+    if (hit) return k * 64 + __ffsll(hit) - 1;
+  }
+  return -1;
+}
+
 // Finds the request that owns logical index `idx`, counting either work units
 // or (kv-head, row tile) groups per request.  Every lane of the wave ends with
 // the same answer.  Returns false when idx is past the end.
@@ -172,13 +192,9 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   int32_t r, node_base, n, L;
   int64_t ubase;
   if (a.plan_count > 0) {
-    // binary search of the dispatch-ordered plan in the kernel arguments
-    int lo = 0, hi = a.plan_count - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (a.plan[mid].unit_end > uid) hi = mid; else lo = mid + 1;
-    }
-    if (a.plan[lo].unit_end <= uid) return;
+    // the dispatch-ordered plan in the kernel arguments
+    const int lo = __builtin_amdgcn_readfirstlane(find_plan_entry(a, uid, false));
+    if (lo < 0) return;
     r = a.plan[lo].request;
     ubase = lo > 0 ? a.plan[lo - 1].unit_end : 0;
     node_base = a.plan[lo].node_base;
@@ -209,8 +225,8 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   const int64_t u = uid - ubase;
   const int32_t tile = (int32_t)(u % tiles);
   const int64_t rest = u / tiles;
-  const int32_t chunk = (int32_t)(rest % chunks);
-  const int32_t g = (int32_t)(rest / chunks);
+  const int32_t g = (int32_t)(rest % a.num_kv_heads);
+  const int32_t chunk = (int32_t)(rest / a.num_kv_heads);
   const int32_t M = n * G;
   const int32_t row0 = tile * RT;
   const int32_t row_end = min(M, row0 + RT);
@@ -613,17 +629,25 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
     return;
   }
 
-  // ---- split prefix: write this chunk's partial (reference max, denominator,
-  // numerator); tree_attn_combine_kernel merges the chunks after this kernel.
+  // ---- split prefix: write this chunk's partial: its own normalised output
+  // in bf16 (a weighted mean of V rows, so bf16 keeps 2^-9 relative
+  // precision), and its reference max and denominator in fp32;
+  // tree_attn_combine_kernel merges the chunks after this kernel.
   if (!wave_live) return;
 #pragma unroll
   for (int rb = 0; rb < 2; ++rb) {
     const int row = wrow0 + rb * 16 + j16;
     if (row >= row_end) continue;
     const int64_t slot = uid * kMaxRowsPerTile + (row - row0);
-    float *wo = a.ws_o + slot * D + q4;
+    const float inv = l_tot[rb] > 0.f ? 1.f / l_tot[rb] : 0.f;
+    __bf16 *wo = a.ws_o + slot * D + q4;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) *(f32x4 *)(wo + dt * 16) = o[rb][dt];
+    for (int dt = 0; dt < DT; ++dt) {
+      u32x2 w;
+      w[0] = pack_bf16x2(o[rb][dt][0] * inv, o[rb][dt][1] * inv);
+      w[1] = pack_bf16x2(o[rb][dt][2] * inv, o[rb][dt][3] * inv);
+      *(u32x2 *)(wo + dt * 16) = w;
+    }
     if (lane < 16) *(f32x2 *)(a.ws_ml + slot * 2) = f32x2{m_ref[rb], l_tot[rb]};
   }
 }
@@ -633,12 +657,8 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
 __device__ __forceinline__ bool group_request(const TreeAttnArgs &a, int64_t gid, int32_t &node_base,
                                               int32_t &n, int32_t &L, int64_t &ubase, int64_t &gbase) {
   if (a.plan_count > 0) {
-    int lo = 0, hi = a.plan_count - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (a.plan[mid].group_end > gid) hi = mid; else lo = mid + 1;
-    }
-    if (a.plan[lo].group_end <= gid) return false;
+    const int lo = __builtin_amdgcn_readfirstlane(find_plan_entry(a, gid, true));
+    if (lo < 0) return false;
     ubase = lo > 0 ? a.plan[lo - 1].unit_end : 0;
     gbase = lo > 0 ? a.plan[lo - 1].group_end : 0;
     node_base = a.plan[lo].node_base;
@@ -655,8 +675,9 @@ __device__ __forceinline__ bool group_request(const TreeAttnArgs &a, int64_t gid
 }
 
 // Merges the chunk partials of every split (request, kv-head, row tile):
-// out = sum_c 2^((m_c - m) c) o_c / sum_c 2^((m_c - m) c) l_c.  One workgroup
-// per 16 rows of a group; each thread owns 8 columns of one row.
+// with w_c = l_c 2^((m_c - m) c), out = sum_c w_c o_c / sum_c w_c, o_c being
+// chunk c's own normalised output.  One workgroup per 16 rows of a group;
+// each thread owns D/16 columns of one row.
 template <int D>
 __global__ __launch_bounds__(kThreads) void tree_attn_combine_kernel(TreeAttnArgs a) {
   constexpr int kRowsPerWg = 16;
@@ -685,17 +706,24 @@ __global__ __launch_bounds__(kThreads) void tree_attn_combine_kernel(TreeAttnArg
   f32x4 acc[CPT / 4];
 #pragma unroll
   for (int k = 0; k < CPT / 4; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
   for (int cc = 0; cc < chunks; ++cc) {
-    const int64_t slot = (ubase + ((int64_t)g * chunks + cc) * tiles + tile) * kMaxRowsPerTile + rl;
+    const int64_t slot = (ubase + ((int64_t)cc * a.num_kv_heads + g) * tiles + tile) * kMaxRowsPerTile + rl;
     const f32x2 ml = *(const f32x2 *)(a.ws_ml + slot * 2);
+    u32x4 raw = {0u, 0u, 0u, 0u};  // CPT bf16 values
+    if (CPT == 8) raw = *(const u32x4 *)(a.ws_o + slot * D + col);
+    else { const u32x2 h = *(const u32x2 *)(a.ws_o + slot * D + col); raw[0] = h[0]; raw[1] = h[1]; }
     const float m_new = fmaxf(mm, ml[0]);
     const float sa = __builtin_amdgcn_exp2f((mm - m_new) * c);
-    const float sb = __builtin_amdgcn_exp2f((ml[0] - m_new) * c);
+    const float wb = ml[1] * __builtin_amdgcn_exp2f((ml[0] - m_new) * c);
     mm = m_new;
-    ll = ll * sa + ml[1] * sb;
+    ll = ll * sa + wb;
 #pragma unroll
-    for (int k = 0; k < CPT / 4; ++k)
-      acc[k] = acc[k] * sa + *(const f32x4 *)(a.ws_o + slot * D + col + 4 * k) * sb;
+    for (int k = 0; k < CPT / 4; ++k) {
+      const f32x4 v = {bf16_bits_to_float(raw[2 * k] & 0xffffu), bf16_bits_to_float(raw[2 * k] >> 16),
+                       bf16_bits_to_float(raw[2 * k + 1] & 0xffffu), bf16_bits_to_float(raw[2 * k + 1] >> 16)};
+      acc[k] = acc[k] * sa + v * wb;
+    }
   }
   const float inv = ll > 0.f ? 1.f / ll : 0.f;
   const int row = tile * RT + rl;
