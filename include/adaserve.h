@@ -96,8 +96,10 @@ size_t adaserve_tree_attn_workspace_bytes(int32_t num_requests, const int32_t *n
  * Supported: dtype F32 or BF16; head_dim 64 or 128; page_size 16; any
  * Hq % Hkv == 0 with Hq / Hkv <= 16; L_r >= 0 (L_r = 0: attention over the
  * root path only).  BF16 computes Q.K^T and P.V on bf16 matrix cores with
- * fp32 accumulation and rounds the output to bf16 (nearest even); F32 computes
- * in fp32 throughout.
+ * fp32 accumulation and rounds the output to bf16 (nearest even); when a
+ * prefix is split into chunks, each chunk's own normalised output is kept in
+ * bf16 and the chunks are merged with fp32 weights.  F32 computes in fp32
+ * throughout.
  * Slots past L_r in the last page and pages not listed for r are never read
  * into the result (they may hold NaN).  Block-table entries outside
  * [0, num_pages) are treated as all-zero pages.  The device arrays must equal
