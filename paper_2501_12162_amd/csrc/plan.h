@@ -17,9 +17,7 @@
 // Units are numbered request by request; inside a request the order is
 // (chunk, g, tile) with the tile fastest, so the tiles that read the same KV
 // chunk are neighbours (and mostly land on one XCD, see xcd_swizzle), and
-// the neighbouring runs of units that an XCD takes cover every kv-head: a
-// kv-head's (page, head) chunks sit at one offset inside every page, and an
-// XCD that read only one head measured markedly slower than the others.
+// the runs of units an XCD takes spread over every kv-head.
 //
 // The host planner and the device-side unit lookup both use the functions
 // below, so their arithmetic cannot drift apart.
