@@ -4,8 +4,8 @@
  * One verification pass of SLO-customised speculative decoding (section 4.3,
  * step 4): the target model scores every node of every request's draft token
  * tree in one pass, and the tokens to commit are read off the logits of those
- * nodes (section 5.1).  The library provides the three steps of that pass
- * that run after the projections:
+ * nodes (section 5.1).  The library provides the steps of that pass that run
+ * after the projections:
  *
  *   adaserve_tree_attn_verify  paged tree attention: each node attends to its
  *                              request's cached prefix plus its own
@@ -13,7 +13,9 @@
  *                              section 3, Theorem 1's root-to-v paths);
  *   adaserve_node_argmax       the target's greedy choice at every node;
  *   adaserve_tree_accept       the longest accepted root path per request and
- *                              the tokens it commits.
+ *                              the tokens it commits;
+ *   adaserve_commit_accepted_kv  the accepted path's keys and values written
+ *                              into the request's paged cache.
  *
  * Conventions for every entry point:
  *  - Pointers without a _host suffix are DEVICE pointers owned by the caller;
@@ -162,6 +164,40 @@ int32_t adaserve_tree_accept(int32_t num_requests, int32_t total_nodes,
                              const int32_t *draft_tokens, const int32_t *target_argmax,
                              int32_t max_accept, int32_t *accept_len, int32_t *accept_tokens,
                              int32_t *accept_nodes, void *stream);
+
+/*
+ * Accepted-path KV commit: the keys and values of the accepted path enter
+ * the request's paged cache, so the next iteration's prefix holds them
+ * (section 5.1: the verified tokens are stored back into the request pool for
+ * the next iteration; section 2: the root is the last generated token, whose
+ * K/V, like every tree node's, was computed in the verification pass).
+ *
+ * For request r with len = accept_len[r] >= 1 and L = prefix_len[r], row
+ * k = 0 .. len-1 copies the tree row of local node accept_nodes[r][k]
+ * (k_tree/v_tree row node_indptr[r] + node, every kv-head) to cache position
+ * L + k: page block_table[r][(L + k) / page_size], slot (L + k) % page_size.
+ * Rows are committed in order up to the first row that cannot be: node
+ * outside [0, N_r), position past the block-table row, or a page id outside
+ * [0, num_pages); nothing at or after that row is written.
+ * new_prefix_len[r] = L + (rows committed).  A request with accept_len < 1
+ * (e.g. -1 from adaserve_tree_accept) or accept_len > max_accept commits
+ * nothing and keeps L.  new_prefix_len may be the prefix_len array itself.
+ * No other byte of k_pages / v_pages is written.
+ *
+ * Layouts as in adaserve_tree_attn_verify: k_tree, v_tree [total_nodes, Hkv,
+ * D]; k_pages, v_pages [num_pages, Hkv, page_size, D]; accept_nodes
+ * [num_requests, max_accept] int32 (device).  dtype F32 or BF16; head_dim * element
+ * size a multiple of 16 bytes; page_size >= 1.  All arrays are device
+ * memory; the copy is bit-exact.
+ */
+int32_t adaserve_commit_accepted_kv(int32_t num_requests, const int32_t *node_indptr,
+                                    const int32_t *accept_len, const int32_t *accept_nodes,
+                                    int32_t max_accept, const void *k_tree, const void *v_tree,
+                                    void *k_pages, void *v_pages, int32_t num_pages,
+                                    const int32_t *block_table, int32_t block_table_stride,
+                                    const int32_t *prefix_len, int32_t num_kv_heads,
+                                    int32_t head_dim, int32_t page_size, int32_t dtype,
+                                    int32_t *new_prefix_len, void *stream);
 
 /* Message describing the last non-OK status returned on this thread. */
 const char *adaserve_last_error(void);

@@ -4,7 +4,9 @@ A plain, slow, obviously correct evaluation (``oracle.c``, fp64, OpenMP)
 of tree attention, per-node argmax and longest-accepted-path acceptance,
 written from the paper's definitions (section 2 draft token trees;
 section 3 Theorem 1 path acceptance; section 4.3 step 4 verification;
-section 5.1 logits returned per node; Appendix B parents before children).
+section 5.1 logits returned per node; Appendix B parents before children),
+plus the accepted-path KV commit (``commit_kv``, plain numpy: section 5.1,
+verified tokens stored back for the next iteration).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  It shares no code with the HIP
@@ -157,3 +159,56 @@ def tree_accept_bruteforce(node_indptr, parent, draft_tokens, target_argmax, max
     """Acceptance by enumerating every root-to-leaf path (same outputs)."""
     return _accept("oracle_tree_accept_bruteforce", node_indptr, parent, draft_tokens,
                    target_argmax, max_accept)
+
+
+def commit_kv(*, node_indptr, accept_len, accept_nodes, k_tree, v_tree, k_pages, v_pages,
+              block_table, prefix_len, page_size: int):
+    """Accepted-path KV commit (section 5.1: the verified tokens are stored back
+    into the request pool for the next iteration; section 2: the root is the
+    last generated token, so the accepted path root..i* is what the next
+    iteration's prefix must hold).
+
+    Reading: request r with len = accept_len[r] >= 1 commits rows k = 0, 1, ...
+    in order: the tree row of local node accept_nodes[r, k] goes to cache
+    position L_r + k (page block_table[r, (L_r + k) // page_size], slot
+    (L_r + k) % page_size), every kv-head, K and V.  The first row whose node
+    is outside the tree, whose position is past the block-table row or whose
+    page id is outside the pool ends the commit.  A request with len < 1 or
+    len > max_accept commits nothing.
+
+    Works on copies: returns ``(k_pages, v_pages, new_prefix_len)`` with
+    new_prefix_len[r] = L_r + rows committed.  Element-wise copies of whatever
+    dtype the arrays hold (bf16 as uint16 bit patterns), so the result is
+    bit-exact by construction.
+    """
+    indptr = np.asarray(node_indptr, dtype=np.int64)
+    alen = np.asarray(accept_len, dtype=np.int64)
+    nodes = np.asarray(accept_nodes, dtype=np.int64)
+    bt = np.asarray(block_table, dtype=np.int64).reshape(len(alen), -1)
+    plen = np.asarray(prefix_len, dtype=np.int64)
+    kp, vp = np.array(k_pages, copy=True), np.array(v_pages, copy=True)
+    num_pages = kp.shape[0]
+    max_accept = nodes.shape[1]
+    new_len = plen.copy()
+    for r in range(len(alen)):
+        n_r = int(indptr[r + 1] - indptr[r])
+        length, L = int(alen[r]), int(plen[r])
+        if length < 1 or length > max_accept or L < 0 or n_r < 1:
+            continue
+        done = 0
+        for k in range(length):
+            node = int(nodes[r, k])
+            t = L + k
+            e = t // page_size
+            if not (0 <= node < n_r) or e >= bt.shape[1]:
+                break
+            page = int(bt[r, e])
+            if not (0 <= page < num_pages):
+                break
+            row = int(indptr[r]) + node
+            kp[page, :, t % page_size, :] = k_tree[row]
+            vp[page, :, t % page_size, :] = v_tree[row]
+            done += 1
+        new_len[r] = L + done
+    return kp, vp, new_len.astype(np.int32)
+

@@ -36,6 +36,8 @@ SIGNATURES = {
                                          _I32, _I32, _I32, _I32, _F32, _I32, _P, _P, _SZ, _P]),
     "adaserve_node_argmax": (_I32, [_P, _I64, _I32, _I32, _I32, _P, _P]),
     "adaserve_tree_accept": (_I32, [_I32, _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _P]),
+    "adaserve_commit_accepted_kv": (_I32, [_I32, _P, _P, _P, _I32, _P, _P, _P, _P, _I32, _P, _I32, _P,
+                                           _I32, _I32, _I32, _I32, _P, _P]),
     "adaserve_last_error": (ctypes.c_char_p, []),
 }
 
@@ -153,4 +155,20 @@ def adaserve_tree_accept(*, node_indptr, parent, draft_tokens, target_argmax, ma
         int(B), int(parent.shape[0]), _dptr(node_indptr), _dptr(parent), _dptr(draft_tokens),
         _dptr(target_argmax), int(max_accept), _dptr(accept_len), _dptr(accept_tokens),
         _dptr(accept_nodes), _stream(stream))
+    _check(st)
+
+
+def adaserve_commit_accepted_kv(*, node_indptr, accept_len, accept_nodes, k_tree, v_tree, k_pages,
+                                v_pages, block_table, prefix_len, new_prefix_len, stream=None) -> None:
+    """Write the accepted paths' K/V rows into the paged cache at L_r .. L_r + len - 1.
+    accept_nodes [B, max_accept]; k_tree/v_tree [T, Hkv, D]; k_pages/v_pages [P, Hkv, ps, D]."""
+    B = node_indptr.shape[0] - 1
+    _, Hkv, D = k_tree.shape
+    P, ps = k_pages.shape[0], k_pages.shape[2]
+    bt_stride = block_table.shape[1] if block_table.dim() == 2 else 0
+    st = load_library().adaserve_commit_accepted_kv(
+        int(B), _dptr(node_indptr), _dptr(accept_len), _dptr(accept_nodes), int(accept_nodes.shape[1]),
+        _dptr(k_tree), _dptr(v_tree), _dptr(k_pages), _dptr(v_pages), int(P), _dptr(block_table),
+        int(bt_stride), _dptr(prefix_len), int(Hkv), int(D), int(ps), _dtype_code(k_tree),
+        _dptr(new_prefix_len), _stream(stream))
     _check(st)

@@ -453,4 +453,54 @@ int32_t adaserve_tree_accept(int32_t num_requests, int32_t total_nodes, const in
                        "accept launch");
 }
 
+int32_t adaserve_commit_accepted_kv(int32_t num_requests, const int32_t *node_indptr, const int32_t *accept_len,
+                                    const int32_t *accept_nodes, int32_t max_accept, const void *k_tree,
+                                    const void *v_tree, void *k_pages, void *v_pages, int32_t num_pages,
+                                    const int32_t *block_table, int32_t block_table_stride,
+                                    const int32_t *prefix_len, int32_t num_kv_heads, int32_t head_dim,
+                                    int32_t page_size, int32_t dtype, int32_t *new_prefix_len, void *stream) {
+  if (num_requests < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_requests %d < 0", num_requests);
+  if (max_accept < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "max_accept %d < 1", max_accept);
+  if (num_pages < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_pages %d < 0", num_pages);
+  if (block_table_stride < 0)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "block_table_stride %d < 0", block_table_stride);
+  if (num_kv_heads < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_kv_heads %d < 1", num_kv_heads);
+  if (head_dim < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "head_dim %d < 1", head_dim);
+  if (page_size < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "page_size %d < 1", page_size);
+  if (dtype != ADASERVE_F32 && dtype != ADASERVE_BF16)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "dtype %d is neither F32 nor BF16", dtype);
+  const int64_t row_bytes = (int64_t)head_dim * (dtype == ADASERVE_BF16 ? 2 : 4);
+  if (row_bytes % 16 != 0 || row_bytes > (1 << 20))
+    return fail(ADASERVE_ERR_UNSUPPORTED, "head_dim * element size = %lld bytes is not a multiple of 16 "
+                "(or exceeds 1 MiB)", (long long)row_bytes);
+  if (num_requests == 0) return ADASERVE_OK;
+  if (!node_indptr || !accept_len || !accept_nodes || !prefix_len || !new_prefix_len)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  if (!k_tree || !v_tree || !k_pages || !v_pages || (block_table_stride > 0 && !block_table))
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  if (!aligned(k_tree, 16) || !aligned(v_tree, 16) || !aligned(k_pages, 16) || !aligned(v_pages, 16))
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "k_tree, v_tree, k_pages and v_pages must be 16-byte aligned");
+  const int32_t st = check_device();
+  if (st != ADASERVE_OK) return st;
+  CommitArgs a;
+  a.num_requests = num_requests;
+  a.node_indptr = node_indptr;
+  a.accept_len = accept_len;
+  a.accept_nodes = accept_nodes;
+  a.max_accept = max_accept;
+  a.k_tree = k_tree;
+  a.v_tree = v_tree;
+  a.k_pages = k_pages;
+  a.v_pages = v_pages;
+  a.num_pages = num_pages;
+  a.block_table = block_table;
+  a.bt_stride = block_table_stride;
+  a.prefix_len = prefix_len;
+  a.num_kv_heads = num_kv_heads;
+  a.row_bytes = (int32_t)row_bytes;
+  a.page_size = page_size;
+  a.new_prefix_len = new_prefix_len;
+  return launch_status(launch_commit_kv(a, (hipStream_t)stream), "commit launch");
+}
+
 }  // extern "C"

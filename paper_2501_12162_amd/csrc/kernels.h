@@ -62,4 +62,26 @@ hipError_t launch_tree_accept(int32_t num_requests, int32_t total_nodes, const i
                               int32_t max_accept, int32_t *accept_len, int32_t *accept_tokens,
                               int32_t *accept_nodes, hipStream_t stream);
 
+struct CommitArgs {
+  int32_t num_requests;
+  const int32_t *node_indptr;
+  const int32_t *accept_len;
+  const int32_t *accept_nodes;   // [num_requests, max_accept]
+  int32_t max_accept;
+  const void *k_tree;
+  const void *v_tree;
+  void *k_pages;
+  void *v_pages;
+  int32_t num_pages;
+  const int32_t *block_table;
+  int32_t bt_stride;
+  const int32_t *prefix_len;
+  int32_t num_kv_heads;
+  int32_t row_bytes;             // head_dim * element size, a multiple of 16
+  int32_t page_size;
+  int32_t *new_prefix_len;
+};
+
+hipError_t launch_commit_kv(const CommitArgs &a, hipStream_t stream);
+
 }  // namespace adaserve

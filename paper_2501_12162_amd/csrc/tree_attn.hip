@@ -39,7 +39,6 @@ namespace adaserve {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kMaxChunkPages = kMaxChunk / kPageSize;
 
 // 16 bytes of zeros: the source of every DMA lane whose key is out of range,
 // so no NaN from an unused page slot reaches LDS.  Its device address is

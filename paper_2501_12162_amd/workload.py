@@ -205,11 +205,15 @@ def make_batch(
     row_pad: int = 0,
     name: str = "custom",
     rng: Optional[np.random.Generator] = None,
+    reserve_tokens: int = 0,
 ) -> VerifyBatch:
     """Draw every tensor of one verify batch for the given tree shapes.
 
     ``parents`` holds one local parent array per request; ``prefix_lens`` the
-    number of tokens already in each request's KV cache.
+    number of tokens already in each request's KV cache.  ``reserve_tokens``
+    extends every request's block table to cover that many positions past its
+    prefix (pages for the accepted path to be committed to; NaN-filled like
+    every slot past the prefix).  With the default 0 nothing changes.
     """
     if dtype not in ("bf16", "f32"):
         raise ValueError("dtype must be 'bf16' or 'f32'")
@@ -230,7 +234,7 @@ def make_batch(
         qkv_std = 1.0 if dtype == "f32" else 1.0 / math.sqrt(head_dim)
 
     # Paged prefix: a shuffled pool with poisoned spare pages.
-    npages_req = [(int(l) + ps - 1) // ps for l in L]
+    npages_req = [(int(l) + int(reserve_tokens) + ps - 1) // ps for l in L]
     live = int(sum(npages_req))
     if extra_pages is None:
         extra_pages = 1 + live // 16
@@ -254,11 +258,11 @@ def make_batch(
     for r in range(B):
         n = npages_req[r]
         owned[block_table[r, :n]] = True
-        tail = int(L[r]) - (n - 1) * ps if n else ps
-        if n and tail < ps:
-            last = block_table[r, n - 1]
-            k_pages[last, :, tail:, :] = nan
-            v_pages[last, :, tail:, :] = nan
+        # every slot from position L_r on (the prefix ends inside page L_r // ps)
+        for e in range(int(L[r]) // ps, n):
+            first = int(L[r]) - e * ps if e == int(L[r]) // ps else 0
+            k_pages[block_table[r, e], :, first:, :] = nan
+            v_pages[block_table[r, e], :, first:, :] = nan
     k_pages[~owned] = nan
     v_pages[~owned] = nan
 

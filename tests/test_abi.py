@@ -132,3 +132,41 @@ def test_accept_rejects_bad_arguments(lib):
     assert f(1, 4, FAKE, None, FAKE, FAKE, 4, FAKE, FAKE, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
     assert f(1, 4, FAKE, FAKE, FAKE, FAKE, 4, None, FAKE, FAKE, None) == ada.ADASERVE_ERR_INVALID_ARGUMENT
     assert f(0, 0, None, None, None, None, 4, None, None, None, None) == ada.ADASERVE_OK
+
+
+def _commit(lib, **kw):
+    args = dict(B=1, indptr=FAKE, alen=FAKE, nodes=FAKE, max_accept=4, k_tree=FAKE, v_tree=FAKE,
+                k_pages=FAKE, v_pages=FAKE, num_pages=4, bt=FAKE, bt_stride=2, plen=FAKE, hkv=2,
+                d=128, ps=16, dtype=ada.ADASERVE_BF16, new_len=FAKE)
+    args.update(kw)
+    return lib.adaserve_commit_accepted_kv(
+        args["B"], args["indptr"], args["alen"], args["nodes"], args["max_accept"], args["k_tree"],
+        args["v_tree"], args["k_pages"], args["v_pages"], args["num_pages"], args["bt"],
+        args["bt_stride"], args["plen"], args["hkv"], args["d"], args["ps"], args["dtype"],
+        args["new_len"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=-1), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(max_accept=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(num_pages=-1), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(bt_stride=-2), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(hkv=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(d=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(ps=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(dtype=3), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(d=12), ada.ADASERVE_ERR_UNSUPPORTED),                               # 24-byte rows
+    (dict(d=6, dtype=ada.ADASERVE_F32), ada.ADASERVE_ERR_UNSUPPORTED),
+    (dict(alen=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(new_len=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(k_pages=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(bt=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(v_tree=FAKE + 8), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+])
+def test_commit_rejects_bad_arguments(lib, kw, code):
+    assert _commit(lib, **kw) == code
+    assert lib.adaserve_last_error()
+
+
+def test_commit_empty_batch_is_a_noop(lib):
+    assert _commit(lib, B=0, indptr=None, alen=None) == ada.ADASERVE_OK

@@ -1,0 +1,89 @@
+"""GPU parity of the accepted-path KV commit (adaserve_commit_accepted_kv)
+against the oracle's commit_kv: the whole K/V page pools and the new prefix
+lengths must match bit for bit (the operation is a copy).  Inputs to both
+sides come from the oracle's acceptance on the same seeded batch."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2501_12162_amd.workload import chain_tree, make_batch, make_config, random_tree
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2501_12162_amd as ada
+    ada.load_library()
+    return torch
+
+
+def _run(torch, b, alen, nodes, in_place=False):
+    import paper_2501_12162_amd as ada
+    dev = torch.device("cuda")
+    dt = torch.bfloat16 if b.dtype == "bf16" else torch.float32
+
+    def t(a, dtype=None):
+        x = torch.from_numpy(np.ascontiguousarray(a))
+        if dtype is torch.bfloat16:
+            x = x.view(torch.bfloat16)
+        return x.to(dev)
+    kt, vt = t(b.k_tree, dt), t(b.v_tree, dt)
+    kp, vp = t(b.k_pages, dt), t(b.v_pages, dt)
+    indptr, bt, plen = t(b.node_indptr), t(b.block_table), t(b.prefix_len)
+    al, nd = t(np.asarray(alen, np.int32)), t(np.asarray(nodes, np.int32))
+    new_len = plen if in_place else torch.empty_like(plen)
+    ada.adaserve_commit_accepted_kv(node_indptr=indptr, accept_len=al, accept_nodes=nd, k_tree=kt,
+                                    v_tree=vt, k_pages=kp, v_pages=vp, block_table=bt, prefix_len=plen,
+                                    new_prefix_len=new_len)
+    torch.cuda.synchronize()
+
+    def back(x):
+        y = x.cpu()
+        return y.view(torch.int16).numpy().view(np.uint16) if y.dtype == torch.bfloat16 else y.numpy()
+    return back(kp), back(vp), new_len.cpu().numpy()
+
+
+def _check(torch, b, alen, nodes, in_place=False):
+    ek, ev, elen = oracle.commit_kv(node_indptr=b.node_indptr, accept_len=alen, accept_nodes=nodes,
+                                    k_tree=b.k_tree, v_tree=b.v_tree, k_pages=b.k_pages,
+                                    v_pages=b.v_pages, block_table=b.block_table,
+                                    prefix_len=b.prefix_len, page_size=b.page_size)
+    gk, gv, glen = _run(torch, b, alen, nodes, in_place)
+    np.testing.assert_array_equal(glen, elen)
+    assert gk.tobytes() == ek.tobytes()
+    assert gv.tobytes() == ev.tobytes()
+    return elen
+
+
+@pytest.mark.parametrize("cfg", [2, 5])
+def test_commit_named_workload_shapes(torch_cuda, cfg):
+    """Trees and prefixes of the named workload (with room reserved past every
+    prefix), acceptance from the oracle."""
+    base = make_config(cfg)
+    parents = [base.parent[base.node_indptr[r]:base.node_indptr[r + 1]] for r in range(base.num_requests)]
+    b = make_batch(parents=parents, prefix_lens=base.prefix_len, num_q_heads=base.num_q_heads,
+                   num_kv_heads=base.num_kv_heads, head_dim=base.head_dim, vocab=64, seed=cfg,
+                   reserve_tokens=40)
+    alen, _, nodes = oracle.tree_accept(b.node_indptr, b.parent, b.draft_tokens, b.planted_argmax, 64)
+    new_len = _check(torch_cuda, b, alen, nodes)
+    assert (new_len == b.prefix_len + alen).all()
+
+
+def test_commit_edge_cases_f32_and_in_place(torch_cuda):
+    """Missing pages mid-path, a node outside its tree, accept_len -1 and 0, a
+    length above max_accept, an empty prefix; new_prefix_len written over
+    prefix_len; fp32 rows (D = 64)."""
+    rng = np.random.Generator(np.random.PCG64(77))
+    parents = [chain_tree(12), chain_tree(12), random_tree(rng, 9, 4), chain_tree(3),
+               chain_tree(5), chain_tree(6), chain_tree(4)]
+    b = make_batch(parents=parents, prefix_lens=[13, 30, 5, 0, 8, 2, 16], num_q_heads=4,
+                   num_kv_heads=2, head_dim=64, dtype="f32", vocab=64, seed=2)
+    M = 8
+    nodes = np.tile(np.arange(M, dtype=np.int32), (7, 1))
+    nodes[4, 2] = 9                       # request 4: node outside its 5-node tree at k = 2
+    alen = np.array([8, 3, -1, 3, 5, 9, 0], np.int32)   # request 5: len > max_accept
+    new_len = _check(torch_cuda, b, alen, nodes, in_place=True)
+    assert new_len.tolist() == [16, 32, 5, 0, 10, 2, 16]   # request 3 has no page at all
