@@ -211,6 +211,30 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
+    # The accepted-path KV commit runs after the step (it is not part of the
+    # verification pass the metric times): its own events, on the last
+    # replica, with the last step's acceptance.  Rows land in slots past each
+    # prefix, which attention never reads.
+    rp = reps[(args.warmup + args.steps - 1) % n_rep]
+    new_len = torch.empty_like(dev.prefix_len)
+    commit_ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def commit():
+        ada.adaserve_commit_accepted_kv(
+            node_indptr=dev.node_indptr, accept_len=dev.accept_len, accept_nodes=dev.accept_nodes,
+            k_tree=rp["k_tree"], v_tree=rp["v_tree"], k_pages=rp["k_pages"], v_pages=rp["v_pages"],
+            block_table=dev.block_table, prefix_len=dev.prefix_len, new_prefix_len=new_len)
+    commit()
+    torch.cuda.synchronize()
+    calib_dst.copy_(calib_src)   # keeps the GPU busy while the host enqueues the timed calls
+    commit_ev[0].record(stream)
+    for _ in range(10):
+        commit()
+    commit_ev[1].record(stream)
+    torch.cuda.synchronize()
+    commit_us = commit_ev[0].elapsed_time(commit_ev[1]) * 1e3 / 10
+    committed_rows = int((new_len - dev.prefix_len).sum().item())
+
     attn_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
     argmax_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
     accept_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
@@ -276,6 +300,9 @@ def main():
             "node_argmax_alg_bytes": costs["argmax_bytes"],
             "tree_accept_us": accept_us,
             "step_event_sum_us": attn_us + argmax_us + accept_us,
+            "kv_commit_us": commit_us,
+            "kv_commit_rows": committed_rows,
+            "kv_commit_bytes": committed_rows * 4 * b.num_kv_heads * b.head_dim * (2 if is_bf16 else 4),
             "path_hbm_frac": (costs["attn_bytes"] + costs["argmax_bytes"])
             / ((attn_us + argmax_us + accept_us) * 1e-6) / 1e9 / HBM_PEAK_GBS,
             "percentiles_us": {

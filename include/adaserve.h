@@ -180,8 +180,8 @@ int32_t adaserve_tree_accept(int32_t num_requests, int32_t total_nodes,
  * outside [0, N_r), position past the block-table row, or a page id outside
  * [0, num_pages); nothing at or after that row is written.
  * new_prefix_len[r] = L + (rows committed).  A request with accept_len < 1
- * (e.g. -1 from adaserve_tree_accept) or accept_len > max_accept commits
- * nothing and keeps L.  new_prefix_len may be the prefix_len array itself.
+ * (e.g. -1 from adaserve_tree_accept), accept_len > max_accept or
+ * accept_len > ADASERVE_MAX_TREE_NODES commits nothing and keeps L.  new_prefix_len may be the prefix_len array itself.
  * No other byte of k_pages / v_pages is written.
  *
  * Layouts as in adaserve_tree_attn_verify: k_tree, v_tree [total_nodes, Hkv,

@@ -173,8 +173,8 @@ def commit_kv(*, node_indptr, accept_len, accept_nodes, k_tree, v_tree, k_pages,
     position L_r + k (page block_table[r, (L_r + k) // page_size], slot
     (L_r + k) % page_size), every kv-head, K and V.  The first row whose node
     is outside the tree, whose position is past the block-table row or whose
-    page id is outside the pool ends the commit.  A request with len < 1 or
-    len > max_accept commits nothing.
+    page id is outside the pool ends the commit.  A request with len < 1,
+    len > max_accept or len > 128 (the tree-size limit) commits nothing.
 
     Works on copies: returns ``(k_pages, v_pages, new_prefix_len)`` with
     new_prefix_len[r] = L_r + rows committed.  Element-wise copies of whatever
@@ -193,7 +193,7 @@ def commit_kv(*, node_indptr, accept_len, accept_nodes, k_tree, v_tree, k_pages,
     for r in range(len(alen)):
         n_r = int(indptr[r + 1] - indptr[r])
         length, L = int(alen[r]), int(plen[r])
-        if length < 1 or length > max_accept or L < 0 or n_r < 1:
+        if length < 1 or length > max_accept or length > 128 or L < 0 or n_r < 1:
             continue
         done = 0
         for k in range(length):
