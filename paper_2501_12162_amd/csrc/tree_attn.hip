@@ -705,7 +705,7 @@ __global__ __launch_bounds__(kThreads) void tree_attn_combine_kernel(TreeAttnArg
   f32x4 acc[CPT / 4];
 #pragma unroll
   for (int k = 0; k < CPT / 4; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
+#pragma unroll 8
   for (int cc = 0; cc < chunks; ++cc) {
     const int64_t slot = (ubase + ((int64_t)cc * a.num_kv_heads + g) * tiles + tile) * kMaxRowsPerTile + rl;
     const f32x2 ml = *(const f32x2 *)(a.ws_ml + slot * 2);
