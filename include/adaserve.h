@@ -15,7 +15,9 @@
  *   adaserve_tree_accept       the longest accepted root path per request and
  *                              the tokens it commits;
  *   adaserve_commit_accepted_kv  the accepted path's keys and values written
- *                              into the request's paged cache.
+ *                              into the request's paged cache;
+ *   adaserve_select_trees      (before the pass) the two selection phases that
+ *                              turn candidate trees into the draft trees.
  *
  * Conventions for every entry point:
  *  - Pointers without a _host suffix are DEVICE pointers owned by the caller;
@@ -198,6 +200,46 @@ int32_t adaserve_commit_accepted_kv(int32_t num_requests, const int32_t *node_in
                                     const int32_t *prefix_len, int32_t num_kv_heads,
                                     int32_t head_dim, int32_t page_size, int32_t dtype,
                                     int32_t *new_prefix_len, void *stream);
+
+/*
+ * Draft-tree selection: the SLO-customised and throughput-optimised selection
+ * phases of Algorithm 2 (section 4.3 steps 2 and 3), run on the candidate
+ * token trees the speculation phase built; the result is the draft token
+ * trees the verification pass scores.
+ *
+ * Request r owns candidates [cand_indptr[r], cand_indptr[r+1]) (root not
+ * included); cand_parent holds LOCAL parents, -1 for a child of the root;
+ * cand_prob is each candidate's path probability f(v).  Every well-formed
+ * request starts with its root (one budget unit).  Requests are visited in
+ * descending order of need (NaN: last; ties by index); each adds its best
+ * remaining candidate while the float32 sum of its added path probabilities
+ * (from 0, in the order added) is below need[r], its tree has fewer than
+ * n_max nodes (root included) and budget remains (section 4.3 step 2; need[r]
+ * is A_cap(r) minus the root's 1).  Then the best remaining candidates of
+ * the whole batch are added while budget remains (step 3).  "Best" is the
+ * highest path probability, ties to the smaller depth (so a parent always
+ * precedes its child and every tree stays connected), then the smaller
+ * request, then the smaller local index.  The budget loops run while
+ * budget > 0 (the printed "B >= 0" would select one node past the budget).
+ *
+ * Outputs: tree_size[r] = nodes selected (root included); row r of
+ * tree_parent / tree_cand ([num_requests, max_nodes] int32) lists the root
+ * first (-1, -1), then the selected candidates by (depth, local index) with
+ * their tree-local parent and their local candidate index; -1 past
+ * tree_size.  These rows are a valid tree for adaserve_tree_attn_verify.
+ * A request with more than 127 candidates, a parent that is not -1 or an
+ * earlier candidate, or a path probability outside (0, 1] or above its
+ * parent's (the root's is 1) takes no part: no budget, tree_size -1, rows of
+ * -1.  If cand_indptr does not start at 0, decreases, or does not end at
+ * num_candidates, every request gets -1.
+ * Limits: num_requests <= 512, num_candidates <= 8192, max_nodes >= 128.
+ * All arrays are device memory.
+ */
+int32_t adaserve_select_trees(int32_t num_requests, int32_t num_candidates,
+                              const int32_t *cand_indptr, const int32_t *cand_parent,
+                              const float *cand_prob, const float *need, int32_t budget,
+                              int32_t n_max, int32_t max_nodes, int32_t *tree_size,
+                              int32_t *tree_parent, int32_t *tree_cand, void *stream);
 
 /* Message describing the last non-OK status returned on this thread. */
 const char *adaserve_last_error(void);

@@ -212,3 +212,107 @@ def commit_kv(*, node_indptr, accept_len, accept_nodes, k_tree, v_tree, k_pages,
         new_len[r] = L + done
     return kp, vp, new_len.astype(np.int32)
 
+
+
+def select_trees(*, cand_indptr, cand_parent, cand_prob, need, budget: int, n_max: int,
+                 max_nodes: int):
+    """SLO-customised selection then throughput-optimised selection
+    (Algorithm 2 after its speculation phase; section 4.3 steps 2 and 3).
+
+    Every request starts with its root (one budget unit each).  Requests are
+    visited in descending order of need (section 4.3 step 2: slower requests
+    first; equal needs keep request order); each adds its best remaining
+    candidate while the added path probabilities sum below need[r], the tree
+    holds fewer than n_max nodes (root included) and budget remains.  Then the
+    best remaining candidates of the whole batch are added while budget
+    remains (step 3).
+
+    Readings: the budget loops run while budget > 0 (the printed `B >= 0`
+    would select one node more than the budget); "best" = highest path
+    probability, ties to the smaller depth (a parent before its child), then
+    (step 3) the smaller request, then the smaller local candidate index; the
+    sum is accumulated in float32 in the order of selection, starting from
+    0 (need[r] excludes the root's 1).  Output trees list the root first, then
+    the selected candidates ordered by (depth, candidate index); tree_parent
+    holds tree-local parents (root -1), tree_cand the candidate index (root -1).
+
+    A request whose candidate tree is malformed -- more than 127 candidates, a
+    parent that is not -1 or an earlier candidate, or a path probability
+    outside (0, 1] or above its parent's (the root's is 1) -- takes no part:
+    no budget, tree_size -1, rows of -1; an index array that does not start at
+    0, decreases, or does not end at the candidate count voids every request.
+    A NaN need asks for nothing and ranks last.
+    """
+    indptr = np.asarray(cand_indptr, dtype=np.int64)
+    par = np.asarray(cand_parent, dtype=np.int64)
+    prob = np.asarray(cand_prob, dtype=np.float32)
+    need = np.asarray(need, dtype=np.float32)
+    need = np.where(np.isnan(need), np.float32(-np.inf), need)   # a NaN need asks for nothing, ranks last
+    B = int(indptr.size - 1)
+    if B > 0 and (indptr[0] != 0 or indptr[-1] != par.size or (np.diff(indptr) < 0).any()):
+        return (np.full(B, -1, np.int32), np.full((B, max_nodes), -1, np.int32),
+                np.full((B, max_nodes), -1, np.int32))
+    depth = np.zeros(par.size, dtype=np.int64)
+    ok = np.ones(B, dtype=bool)
+    for r in range(B):
+        lo, hi = int(indptr[r]), int(indptr[r + 1])
+        if hi - lo > 127 or hi < lo:
+            ok[r] = False
+            continue
+        for i in range(lo, hi):
+            p = int(par[i])
+            fp = np.float32(1.0) if p == -1 else (prob[lo + p] if 0 <= p < i - lo else None)
+            if fp is None or not (np.float32(0) < prob[i] <= fp):
+                ok[r] = False
+                break
+            depth[i] = 1 if p < 0 else depth[lo + p] + 1
+    added = np.zeros(par.size, dtype=bool)
+    for r in range(B):           # candidates of malformed requests are never eligible
+        if not ok[r]:
+            added[int(indptr[r]):int(indptr[r + 1])] = True
+    size = np.ones(B, dtype=np.int64)
+    left = int(budget) - int(ok.sum())
+
+    def best(cands):
+        # highest probability; ties: smaller depth, then the lower index
+        return min(cands, key=lambda i: (-float(prob[i]), int(depth[i]), i)) if cands else None
+
+    order = sorted((r for r in range(B) if ok[r]), key=lambda r: (-float(need[r]), r))
+    for r in order:
+        acc = np.float32(0.0)
+        while acc < need[r] and size[r] < n_max and left > 0:
+            v = best([i for i in range(int(indptr[r]), int(indptr[r + 1])) if not added[i]])
+            if v is None:
+                break
+            added[v] = True
+            size[r] += 1
+            acc = np.float32(acc + prob[v])
+            left -= 1
+    while left > 0:
+        rest = [i for i in range(par.size) if not added[i]]
+        if not rest:
+            break
+        v = best(rest)               # global index order = (request, local index)
+        added[v] = True
+        size[int(np.searchsorted(indptr, v, side="right") - 1)] += 1
+        left -= 1
+
+    tree_size = np.zeros(B, dtype=np.int32)
+    tree_parent = np.full((B, max_nodes), -1, dtype=np.int32)
+    tree_cand = np.full((B, max_nodes), -1, dtype=np.int32)
+    for r in range(B):
+        if not ok[r]:
+            tree_size[r] = -1
+            continue
+        lo = int(indptr[r])
+        sel = [i for i in range(lo, int(indptr[r + 1])) if added[i]]
+        sel.sort(key=lambda i: (int(depth[i]), i))
+        if 1 + len(sel) > max_nodes:
+            raise ValueError("max_nodes too small")
+        tid = {i: k + 1 for k, i in enumerate(sel)}
+        tree_size[r] = 1 + len(sel)
+        for i in sel:
+            p = int(par[i])
+            tree_parent[r, tid[i]] = 0 if p < 0 else tid[lo + p]
+            tree_cand[r, tid[i]] = i - lo
+    return tree_size, tree_parent, tree_cand

@@ -38,6 +38,7 @@ SIGNATURES = {
     "adaserve_tree_accept": (_I32, [_I32, _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _P]),
     "adaserve_commit_accepted_kv": (_I32, [_I32, _P, _P, _P, _I32, _P, _P, _P, _P, _I32, _P, _I32, _P,
                                            _I32, _I32, _I32, _I32, _P, _P]),
+    "adaserve_select_trees": (_I32, [_I32, _I32, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P]),
     "adaserve_last_error": (ctypes.c_char_p, []),
 }
 
@@ -172,3 +173,15 @@ def adaserve_commit_accepted_kv(*, node_indptr, accept_len, accept_nodes, k_tree
         int(bt_stride), _dptr(prefix_len), int(Hkv), int(D), int(ps), _dtype_code(k_tree),
         _dptr(new_prefix_len), _stream(stream))
     _check(st)
+
+
+def adaserve_select_trees(*, cand_indptr, cand_parent, cand_prob, need, budget: int, n_max: int,
+                          tree_size, tree_parent, tree_cand, stream=None) -> None:
+    """Draft trees from candidate trees (tree_parent / tree_cand [B, max_nodes], max_nodes >= 128)."""
+    B = cand_indptr.shape[0] - 1
+    st = load_library().adaserve_select_trees(
+        int(B), int(cand_prob.shape[0]), _dptr(cand_indptr), _dptr(cand_parent), _dptr(cand_prob),
+        _dptr(need), int(budget), int(n_max), int(tree_parent.shape[1]), _dptr(tree_size),
+        _dptr(tree_parent), _dptr(tree_cand), _stream(stream))
+    _check(st)
+

@@ -503,4 +503,41 @@ int32_t adaserve_commit_accepted_kv(int32_t num_requests, const int32_t *node_in
   return launch_status(launch_commit_kv(a, (hipStream_t)stream), "commit launch");
 }
 
+int32_t adaserve_select_trees(int32_t num_requests, int32_t num_candidates, const int32_t *cand_indptr,
+                              const int32_t *cand_parent, const float *cand_prob, const float *need,
+                              int32_t budget, int32_t n_max, int32_t max_nodes, int32_t *tree_size,
+                              int32_t *tree_parent, int32_t *tree_cand, void *stream) {
+  if (num_requests < 0 || num_requests > kSelectMaxRequests)
+    return fail(num_requests < 0 ? ADASERVE_ERR_INVALID_ARGUMENT : ADASERVE_ERR_UNSUPPORTED,
+                "num_requests %d outside [0, %d]", num_requests, kSelectMaxRequests);
+  if (num_candidates < 0 || num_candidates > kSelectMaxCandidates)
+    return fail(num_candidates < 0 ? ADASERVE_ERR_INVALID_ARGUMENT : ADASERVE_ERR_UNSUPPORTED,
+                "num_candidates %d outside [0, %d]", num_candidates, kSelectMaxCandidates);
+  if (budget < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "budget %d < 0", budget);
+  if (n_max < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "n_max %d < 1", n_max);
+  if (max_nodes < ADASERVE_MAX_TREE_NODES)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "max_nodes %d < %d", max_nodes, ADASERVE_MAX_TREE_NODES);
+  if (num_requests == 0) return ADASERVE_OK;
+  if (!cand_indptr || !need || !tree_size || !tree_parent || !tree_cand)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  if (num_candidates > 0 && (!cand_parent || !cand_prob))
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  const int32_t st = check_device();
+  if (st != ADASERVE_OK) return st;
+  SelectArgs a;
+  a.num_requests = num_requests;
+  a.num_candidates = num_candidates;
+  a.cand_indptr = cand_indptr;
+  a.cand_parent = cand_parent;
+  a.cand_prob = cand_prob;
+  a.need = need;
+  a.budget = budget;
+  a.n_max = n_max;
+  a.max_nodes = max_nodes;
+  a.tree_size = tree_size;
+  a.tree_parent = tree_parent;
+  a.tree_cand = tree_cand;
+  return launch_status(launch_select_trees(a, (hipStream_t)stream), "select launch");
+}
+
 }  // extern "C"

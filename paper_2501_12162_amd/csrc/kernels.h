@@ -84,4 +84,25 @@ struct CommitArgs {
 
 hipError_t launch_commit_kv(const CommitArgs &a, hipStream_t stream);
 
+constexpr int kSelectMaxCandidates = 8192;  // per batch
+constexpr int kSelectMaxRequests = 512;
+constexpr int kSelectMaxPerRequest = 127;   // trees of at most 128 nodes
+
+struct SelectArgs {
+  int32_t num_requests;
+  int32_t num_candidates;
+  const int32_t *cand_indptr;   // [num_requests + 1]
+  const int32_t *cand_parent;   // [num_candidates] local: -1 = child of the root
+  const float *cand_prob;       // [num_candidates] path probabilities
+  const float *need;            // [num_requests]
+  int32_t budget;
+  int32_t n_max;
+  int32_t max_nodes;            // output row stride, >= 128
+  int32_t *tree_size;           // [num_requests]
+  int32_t *tree_parent;         // [num_requests, max_nodes]
+  int32_t *tree_cand;           // [num_requests, max_nodes]
+};
+
+hipError_t launch_select_trees(const SelectArgs &a, hipStream_t stream);
+
 }  // namespace adaserve

@@ -404,3 +404,82 @@ def make_tie_logits(rng: np.random.Generator, rows: int, vocab: int, dtype: str 
     if row_pad:
         logits[:, vocab:] = BF16_NAN if dtype == "bf16" else np.float32(np.nan)
     return logits, positions
+
+
+# ---------------------------------------------------------------------------
+# Candidate token trees for the selection phases
+# ---------------------------------------------------------------------------
+
+@dataclass
+class CandidateBatch:
+    """Speculation output for a batch: every request's candidate token tree
+    (root excluded), with each candidate's path probability, plus the
+    selection inputs.
+
+    cand_parent holds LOCAL parents: -1 for a child of the root, else the
+    index of an earlier candidate of the same request.  need[r] is the sum of
+    path probabilities the request's added nodes must reach (A_cap(r) minus
+    the root's 1).  budget counts every selected node, the roots included.
+    """
+    cand_indptr: np.ndarray   # [B + 1] int32
+    cand_parent: np.ndarray   # [C] int32
+    cand_prob: np.ndarray     # [C] float32, in (0, 1]
+    need: np.ndarray          # [B] float32
+    budget: int
+    n_max: int
+    depth: int
+    width: int
+
+    @property
+    def num_requests(self) -> int:
+        return int(self.cand_indptr.size - 1)
+
+
+def make_candidates(rng: np.random.Generator, num_requests: int, depth: int, width: int,
+                    budget: Optional[int] = None, n_max: Optional[int] = None,
+                    prob_levels: Optional[int] = None) -> CandidateBatch:
+    """Beam-search-shaped candidate trees (section 4.3 step 1): depth layers
+    of `width` candidates, each layer's parents drawn from the layer above
+    (higher path probability more likely), each layer ordered by path
+    probability.  Conditional probabilities are uniform in (0, 1]; with
+    `prob_levels` they are multiples of 1/prob_levels (ties on purpose).
+    need[r] ~ U[0, depth] (an A_cap(r) between 1 and depth + 1)."""
+    indptr = [0]
+    parents, probs = [], []
+    for _ in range(num_requests):
+        f_prev = np.ones(1)
+        base = 0
+        p_req, f_req = [], []
+        for layer in range(depth):
+            if layer == 0:
+                par = np.full(width, -1, dtype=np.int64)
+                f_par = np.ones(width)
+            else:
+                w_prev = f_prev / f_prev.sum()
+                pick = rng.choice(f_prev.size, size=width, p=w_prev)
+                par = base + pick
+                f_par = f_prev[pick]
+            if prob_levels:
+                cond = rng.integers(1, prob_levels + 1, size=width) / prob_levels
+            else:
+                cond = 1.0 - rng.random(width)          # (0, 1]
+            f = (f_par * cond).astype(np.float32).astype(np.float64)
+            order = np.argsort(-f, kind="stable")
+            par, f = par[order], f[order]
+            if layer > 0:
+                base += f_prev.size
+            p_req.append(par)
+            f_req.append(f)
+            f_prev = f
+        parents.append(np.concatenate(p_req).astype(np.int32))
+        probs.append(np.concatenate(f_req).astype(np.float32))
+        indptr.append(indptr[-1] + depth * width)
+    need = (rng.random(num_requests) * depth).astype(np.float32)
+    if budget is None:
+        budget = num_requests * (1 + depth * width // 2)
+    if n_max is None:
+        n_max = 1 + depth * width
+    return CandidateBatch(cand_indptr=np.asarray(indptr, dtype=np.int32),
+                          cand_parent=np.concatenate(parents) if parents else np.zeros(0, np.int32),
+                          cand_prob=np.concatenate(probs) if probs else np.zeros(0, np.float32),
+                          need=need, budget=int(budget), n_max=int(n_max), depth=depth, width=width)

@@ -170,3 +170,33 @@ def test_commit_rejects_bad_arguments(lib, kw, code):
 
 def test_commit_empty_batch_is_a_noop(lib):
     assert _commit(lib, B=0, indptr=None, alen=None) == ada.ADASERVE_OK
+
+
+def _select(lib, **kw):
+    args = dict(B=2, C=10, indptr=FAKE, par=FAKE, prob=FAKE, need=FAKE, budget=8, n_max=4,
+                max_nodes=128, size=FAKE, tpar=FAKE, tcand=FAKE)
+    args.update(kw)
+    return lib.adaserve_select_trees(args["B"], args["C"], args["indptr"], args["par"], args["prob"],
+                                     args["need"], args["budget"], args["n_max"], args["max_nodes"],
+                                     args["size"], args["tpar"], args["tcand"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=-1), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(B=513), ada.ADASERVE_ERR_UNSUPPORTED),
+    (dict(C=-1), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(C=8193), ada.ADASERVE_ERR_UNSUPPORTED),
+    (dict(budget=-1), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(n_max=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(max_nodes=127), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(indptr=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(prob=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(tcand=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+])
+def test_select_rejects_bad_arguments(lib, kw, code):
+    assert _select(lib, **kw) == code
+    assert lib.adaserve_last_error()
+
+
+def test_select_empty_batch_is_a_noop(lib):
+    assert _select(lib, B=0, C=0, indptr=None, par=None, prob=None) == ada.ADASERVE_OK
