@@ -235,6 +235,33 @@ def main():
     commit_us = commit_ev[0].elapsed_time(commit_ev[1]) * 1e3 / 10
     committed_rows = int((new_len - dev.prefix_len).sum().item())
 
+    # Draft-tree selection (before a pass; not part of the timed step): a
+    # candidate batch of the workload's request count, depth 8 x beam width 8,
+    # with the workload's total tree size as the budget.
+    from paper_2501_12162_amd.workload import make_candidates
+    cands = make_candidates(np.random.Generator(np.random.PCG64(args.workload)), b.num_requests, 8, 8,
+                            budget=b.total_nodes)
+    tdev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    c_ip, c_par, c_prob, c_need = (tdev(cands.cand_indptr), tdev(cands.cand_parent),
+                                   tdev(cands.cand_prob), tdev(cands.need))
+    s_size = torch.empty(b.num_requests, dtype=torch.int32, device="cuda")
+    s_par = torch.empty(b.num_requests, 128, dtype=torch.int32, device="cuda")
+    s_cand = torch.empty_like(s_par)
+
+    def select():
+        ada.adaserve_select_trees(cand_indptr=c_ip, cand_parent=c_par, cand_prob=c_prob, need=c_need,
+                                  budget=cands.budget, n_max=cands.n_max, tree_size=s_size,
+                                  tree_parent=s_par, tree_cand=s_cand)
+    select()
+    torch.cuda.synchronize()
+    calib_dst.copy_(calib_src)
+    commit_ev[0].record(stream)
+    for _ in range(10):
+        select()
+    commit_ev[1].record(stream)
+    torch.cuda.synchronize()
+    select_us = commit_ev[0].elapsed_time(commit_ev[1]) * 1e3 / 10
+
     attn_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
     argmax_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
     accept_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
@@ -303,6 +330,8 @@ def main():
             "kv_commit_us": commit_us,
             "kv_commit_rows": committed_rows,
             "kv_commit_bytes": committed_rows * 4 * b.num_kv_heads * b.head_dim * (2 if is_bf16 else 4),
+            "select_us": select_us,
+            "select_candidates": int(cands.cand_prob.size),
             "path_hbm_frac": (costs["attn_bytes"] + costs["argmax_bytes"])
             / ((attn_us + argmax_us + accept_us) * 1e-6) / 1e9 / HBM_PEAK_GBS,
             "percentiles_us": {
