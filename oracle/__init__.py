@@ -6,7 +6,9 @@ written from the paper's definitions (section 2 draft token trees;
 section 3 Theorem 1 path acceptance; section 4.3 step 4 verification;
 section 5.1 logits returned per node; Appendix B parents before children),
 plus the accepted-path KV commit (``commit_kv``, plain numpy: section 5.1,
-verified tokens stored back for the next iteration).
+verified tokens stored back for the next iteration), the two selection
+phases of Algorithm 2 (``select_trees``, section 4.3 steps 2-3) and one
+beam-search speculation step (``beam_step``, section 4.3 step 1).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  It shares no code with the HIP
@@ -316,3 +318,54 @@ def select_trees(*, cand_indptr, cand_parent, cand_prob, need, budget: int, n_ma
             tree_parent[r, tid[i]] = 0 if p < 0 else tid[lo + p]
             tree_cand[r, tid[i]] = i - lo
     return tree_size, tree_parent, tree_cand
+
+
+def beam_log_path_prob(logits, beam_logprob):
+    """Log path probability of every child of every beam node (section 4.3
+    step 1): log f(child) = log f(beam) + log softmax(draft logits of the
+    beam)[token], in float64.  logits [B, w_in, V] (float values),
+    beam_logprob [B, w_in].  A row with no finite logit, or a beam of log
+    path probability -inf, has only children of probability 0 (-inf)."""
+    x = np.asarray(logits, dtype=np.float64)
+    lp = np.asarray(beam_logprob, dtype=np.float64)
+    m = x.max(axis=2, keepdims=True)
+    dead = ~np.isfinite(m)
+    m = np.where(dead, 0.0, m)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        lse = m + np.log(np.exp(x - m).sum(axis=2, keepdims=True))
+        score = lp[:, :, None] + (x - lse)
+    return np.where(dead, -np.inf, score)
+
+
+def beam_step(*, logits, beam_logprob, w_out: int):
+    """One beam-search speculation step (section 4.3 step 1): every beam node b
+    of a request expands into all |V| tokens with path probability
+    f(b) * softmax(draft logits of b)[t]; the w_out children with the highest
+    path probability are kept.
+
+    logits: [B, w_in, V] (float32 values; bf16 bit patterns are widened by
+    the caller); beam_logprob: [B, w_in] natural-log path probabilities of the
+    beam nodes (-inf for an unused slot).  Scores come from
+    beam_log_path_prob (float64).
+    Reading: ties go to the smaller beam index, then the smaller token id;
+    outputs are sorted best first; children of path probability 0 (log -inf)
+    are never kept, and slots past the last kept child hold parent -1,
+    token -1, logprob -inf.  Returns (parent [B, w_out] int32, token
+    [B, w_out] int32, logprob [B, w_out] float64).
+    """
+    score = beam_log_path_prob(logits, beam_logprob)       # [B, w_in, V]
+    B, w_in, V = score.shape
+    parent = np.full((B, w_out), -1, np.int32)
+    token = np.full((B, w_out), -1, np.int32)
+    out = np.full((B, w_out), -np.inf, np.float64)
+    bb, tt = np.meshgrid(np.arange(w_in), np.arange(V), indexing="ij")
+    for r in range(B):
+        s = score[r].ravel()
+        # lexicographic: highest score, then smaller beam, then smaller token
+        order = np.lexsort((tt.ravel(), bb.ravel(), -s))[:w_out]
+        order = order[np.isfinite(s[order])]
+        k = order.size
+        parent[r, :k] = bb.ravel()[order]
+        token[r, :k] = tt.ravel()[order]
+        out[r, :k] = s[order]
+    return parent, token, out
