@@ -65,6 +65,10 @@ def algorithmic_costs(b):
                 accept_bytes=accept_bytes)
 
 
+def is_bf16_in(b):
+    return b.dtype == "bf16"
+
+
 def make_replicas(dev, count):
     """``count`` device copies of the per-step input tensors (copy 0 = originals)."""
     reps = [dict(q=dev.q, k_tree=dev.k_tree, v_tree=dev.v_tree, k_pages=dev.k_pages,
@@ -262,6 +266,40 @@ def main():
     torch.cuda.synchronize()
     select_us = commit_ev[0].elapsed_time(commit_ev[1]) * 1e3 / 10
 
+    # One beam-search speculation step (before selection; not part of the
+    # timed step): draft logits of the workload's requests x 8 beams over
+    # the workload's vocabulary, keeping 8 children per request.  Calls cycle
+    # through enough copies of the logits that none is read from the MALL.
+    from paper_2501_12162_amd.workload import make_beam_batch
+    bb = make_beam_batch(np.random.Generator(np.random.PCG64(100 + args.workload)), b.num_requests, 8,
+                         b.vocab, dtype=b.dtype)
+    beam_bytes = bb.logits.nbytes
+    beam_reps = max(2, math.ceil(3 * MALL_BYTES / beam_bytes) + 1)
+    bl = torch.from_numpy(bb.logits.view(np.int16) if is_bf16_in(b) else bb.logits).cuda()
+    if is_bf16_in(b):
+        bl = bl.view(torch.bfloat16)
+    beam_logits = [bl] + [bl.clone() for _ in range(beam_reps - 1)]
+    beam_lp = tdev(bb.beam_logprob)
+    code = ada.ADASERVE_BF16 if is_bf16_in(b) else ada.ADASERVE_F32
+    beam_ws = torch.empty(ada.adaserve_beam_step_workspace_bytes(b.num_requests, 8, b.vocab, 8, code),
+                          dtype=torch.uint8, device="cuda")
+    b_par = torch.empty(b.num_requests, 8, dtype=torch.int32, device="cuda")
+    b_tok = torch.empty_like(b_par)
+    b_lp = torch.empty(b.num_requests, 8, dtype=torch.float32, device="cuda")
+
+    def beam(i):
+        ada.adaserve_beam_step(logits=beam_logits[i % beam_reps], vocab=b.vocab, beam_logprob=beam_lp,
+                               out_parent=b_par, out_token=b_tok, out_logprob=b_lp, workspace=beam_ws)
+    beam(0)
+    torch.cuda.synchronize()
+    calib_dst.copy_(calib_src)
+    commit_ev[0].record(stream)
+    for i in range(20):
+        beam(i + 1)
+    commit_ev[1].record(stream)
+    torch.cuda.synchronize()
+    beam_us = commit_ev[0].elapsed_time(commit_ev[1]) * 1e3 / 20
+
     attn_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
     argmax_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
     accept_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
@@ -332,6 +370,9 @@ def main():
             "kv_commit_bytes": committed_rows * 4 * b.num_kv_heads * b.head_dim * (2 if is_bf16 else 4),
             "select_us": select_us,
             "select_candidates": int(cands.cand_prob.size),
+            "beam_step_us": beam_us,
+            "beam_step_rows": int(bb.logits.shape[0]),
+            "beam_step_hbm_frac": beam_bytes / (beam_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
             "path_hbm_frac": (costs["attn_bytes"] + costs["argmax_bytes"])
             / ((attn_us + argmax_us + accept_us) * 1e-6) / 1e9 / HBM_PEAK_GBS,
             "percentiles_us": {

@@ -17,7 +17,9 @@
  *   adaserve_commit_accepted_kv  the accepted path's keys and values written
  *                              into the request's paged cache;
  *   adaserve_select_trees      (before the pass) the two selection phases that
- *                              turn candidate trees into the draft trees.
+ *                              turn candidate trees into the draft trees;
+ *   adaserve_beam_step         (before selection) one beam-search step of the
+ *                              speculation phase that grows the candidate trees.
  *
  * Conventions for every entry point:
  *  - Pointers without a _host suffix are DEVICE pointers owned by the caller;
@@ -240,6 +242,52 @@ int32_t adaserve_select_trees(int32_t num_requests, int32_t num_candidates,
                               const float *cand_prob, const float *need, int32_t budget,
                               int32_t n_max, int32_t max_nodes, int32_t *tree_size,
                               int32_t *tree_parent, int32_t *tree_cand, void *stream);
+
+/*
+ * One beam-search speculation step (section 4.3 step 1): every beam node of
+ * a request expands into all vocabulary tokens, a child's path probability
+ * being the beam's path probability times the draft model's softmax
+ * probability of the token (section 4.2's product of draft probabilities
+ * along the path), and each request keeps the beam_out children with the
+ * highest path probability.  The first step has one beam per request (the
+ * root, log path probability 0); later steps have beam_in = the previous
+ * step's beam_out.
+ *
+ * Row b of request r is logits row r * beam_in + b: the draft model's logits
+ * after beam node b, columns 0 .. vocab - 1 (row_stride elements apart; the
+ * rest of a row is never read).  beam_logprob [num_requests * beam_in]
+ * holds each beam's natural-log path probability; -inf marks an unused beam
+ * slot, whose logits row is not read.  A child's score is
+ *   beam_logprob[b] + x[b, t] - log(sum over t' of exp(x[b, t'])),
+ * computed in fp32 (the log-sum-exp over the row accumulated in fp32).
+ * Children are ranked by score (higher first), ties to the smaller beam, then
+ * the smaller token (children of one beam whose fp32 scores coincide only
+ * through rounding keep the order of their logits); the beam_out best
+ * children with a finite score are written best first to row r of
+ *   out_parent  [num_requests, beam_out] int32  beam index in [0, beam_in)
+ *   out_token   [num_requests, beam_out] int32  token id in [0, vocab)
+ *   out_logprob [num_requests, beam_out] fp32   the child's score
+ * and slots past them hold -1, -1, -inf.  Logits are finite or -inf (a -inf
+ * logit is a token of probability 0, never kept); NaN or +inf logits give
+ * unspecified (in-range) outputs.
+ *
+ * dtype F32 or BF16 logits; logits 16-byte aligned and row_stride * element
+ * size a multiple of 16 bytes; 1 <= beam_in, beam_out <= 64; vocab <= 2^20
+ * (ADASERVE_ERR_UNSUPPORTED above).  workspace: at
+ * least adaserve_beam_step_workspace_bytes(...) bytes of device memory,
+ * 256-byte aligned, no initialisation needed; calls sharing a workspace must
+ * not overlap in time.  Two kernels are enqueued on `stream` (a scan of
+ * every live logits row, then a per-request merge).  num_requests = 0 is a
+ * no-op.
+ */
+size_t adaserve_beam_step_workspace_bytes(int32_t num_requests, int32_t beam_in, int32_t vocab,
+                                          int32_t beam_out, int32_t dtype);
+
+int32_t adaserve_beam_step(int32_t num_requests, int32_t beam_in, const void *logits,
+                           int64_t row_stride, int32_t vocab, int32_t dtype,
+                           const float *beam_logprob, int32_t beam_out, int32_t *out_parent,
+                           int32_t *out_token, float *out_logprob, void *workspace,
+                           size_t workspace_bytes, void *stream);
 
 /* Message describing the last non-OK status returned on this thread. */
 const char *adaserve_last_error(void);

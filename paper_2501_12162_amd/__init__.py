@@ -39,6 +39,8 @@ SIGNATURES = {
     "adaserve_commit_accepted_kv": (_I32, [_I32, _P, _P, _P, _I32, _P, _P, _P, _P, _I32, _P, _I32, _P,
                                            _I32, _I32, _I32, _I32, _P, _P]),
     "adaserve_select_trees": (_I32, [_I32, _I32, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P]),
+    "adaserve_beam_step_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, _I32]),
+    "adaserve_beam_step": (_I32, [_I32, _I32, _P, _I64, _I32, _I32, _P, _I32, _P, _P, _P, _P, _SZ, _P]),
     "adaserve_last_error": (ctypes.c_char_p, []),
 }
 
@@ -185,3 +187,28 @@ def adaserve_select_trees(*, cand_indptr, cand_parent, cand_prob, need, budget: 
         _dptr(tree_parent), _dptr(tree_cand), _stream(stream))
     _check(st)
 
+
+
+def adaserve_beam_step_workspace_bytes(num_requests: int, beam_in: int, vocab: int, beam_out: int,
+                                       dtype: int) -> int:
+    n = load_library().adaserve_beam_step_workspace_bytes(int(num_requests), int(beam_in), int(vocab),
+                                                          int(beam_out), int(dtype))
+    if n == ctypes.c_size_t(-1).value:
+        _check(ADASERVE_ERR_INVALID_ARGUMENT)
+    return int(n)
+
+
+def adaserve_beam_step(*, logits, vocab: int, beam_logprob, out_parent, out_token, out_logprob,
+                       workspace, stream=None) -> None:
+    """One beam-search step.  logits [num_requests * beam_in, row_stride];
+    beam_logprob [num_requests, beam_in] float32; outputs [num_requests, beam_out]."""
+    B, w_in = beam_logprob.shape
+    rows, stride = logits.shape
+    if rows != B * w_in:
+        raise ValueError("logits has %d rows, beam_logprob asks for %d" % (rows, B * w_in))
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = load_library().adaserve_beam_step(
+        int(B), int(w_in), _dptr(logits), int(stride), int(vocab), _dtype_code(logits), _dptr(beam_logprob),
+        int(out_parent.shape[1]), _dptr(out_parent), _dptr(out_token), _dptr(out_logprob), _dptr(workspace),
+        int(ws_bytes), _stream(stream))
+    _check(st)

@@ -326,6 +326,32 @@ void fill_plan_table(TreeAttnArgs &a, int32_t B, const int32_t *indptr_host, con
 
 }  // namespace
 
+// Beam step: scalar validation shared by the workspace query and the call.
+// On success `parts` is the number of scan workgroups per row and `bytes`
+// the workspace size ((max, sum) pairs, then the per-part sorted lists).
+int32_t validate_beam_shape(int32_t num_requests, int32_t beam_in, int32_t vocab, int32_t beam_out,
+                            int32_t dtype, int32_t &parts, size_t &bytes) {
+  if (num_requests < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_requests %d < 0", num_requests);
+  if (beam_in < 1 || beam_in > kBeamMaxWidth)
+    return fail(beam_in < 1 ? ADASERVE_ERR_INVALID_ARGUMENT : ADASERVE_ERR_UNSUPPORTED,
+                "beam_in %d outside [1, %d]", beam_in, kBeamMaxWidth);
+  if (beam_out < 1 || beam_out > kBeamMaxWidth)
+    return fail(beam_out < 1 ? ADASERVE_ERR_INVALID_ARGUMENT : ADASERVE_ERR_UNSUPPORTED,
+                "beam_out %d outside [1, %d]", beam_out, kBeamMaxWidth);
+  if (vocab < 1 || vocab > kBeamMaxVocab)
+    return fail(vocab < 1 ? ADASERVE_ERR_INVALID_ARGUMENT : ADASERVE_ERR_UNSUPPORTED, "vocab %d outside [1, %d]",
+                vocab, kBeamMaxVocab);
+  if (dtype != ADASERVE_F32 && dtype != ADASERVE_BF16)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "dtype %d is neither F32 nor BF16", dtype);
+  parts = beam_parts(vocab, dtype == ADASERVE_BF16);
+  const int64_t rows = (int64_t)num_requests * beam_in;
+  if (rows * parts > INT32_MAX || (int64_t)num_requests * beam_out > INT32_MAX)
+    return fail(ADASERVE_ERR_UNSUPPORTED, "%lld logit rows of %d entries exceed the launch limit", (long long)rows,
+                vocab);
+  bytes = rows == 0 ? 0 : round_up((size_t)(rows * parts) * 8, 256) + (size_t)(rows * parts) * beam_out * 8;
+  return ADASERVE_OK;
+}
+
 extern "C" {
 
 const char *adaserve_last_error(void) { return g_last_error.c_str(); }
@@ -538,6 +564,57 @@ int32_t adaserve_select_trees(int32_t num_requests, int32_t num_candidates, cons
   a.tree_parent = tree_parent;
   a.tree_cand = tree_cand;
   return launch_status(launch_select_trees(a, (hipStream_t)stream), "select launch");
+}
+
+size_t adaserve_beam_step_workspace_bytes(int32_t num_requests, int32_t beam_in, int32_t vocab, int32_t beam_out,
+                                          int32_t dtype) {
+  int32_t parts = 0;
+  size_t bytes = 0;
+  if (validate_beam_shape(num_requests, beam_in, vocab, beam_out, dtype, parts, bytes) != ADASERVE_OK)
+    return SIZE_MAX;
+  return bytes;
+}
+
+int32_t adaserve_beam_step(int32_t num_requests, int32_t beam_in, const void *logits, int64_t row_stride,
+                           int32_t vocab, int32_t dtype, const float *beam_logprob, int32_t beam_out,
+                           int32_t *out_parent, int32_t *out_token, float *out_logprob, void *workspace,
+                           size_t workspace_bytes, void *stream) {
+  int32_t parts = 0;
+  size_t need = 0;
+  const int32_t v = validate_beam_shape(num_requests, beam_in, vocab, beam_out, dtype, parts, need);
+  if (v != ADASERVE_OK) return v;
+  if (row_stride < vocab)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "row_stride %lld < vocab %d", (long long)row_stride, vocab);
+  if (num_requests == 0) return ADASERVE_OK;
+  if (!logits || !beam_logprob || !out_parent || !out_token || !out_logprob)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  const int64_t esz = dtype == ADASERVE_BF16 ? 2 : 4;
+  if (!aligned(logits, 16) || (row_stride * esz) % 16 != 0)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "logits must be 16-byte aligned with rows a multiple of 16 bytes apart");
+  if (!aligned(beam_logprob, 4) || !aligned(out_parent, 4) || !aligned(out_token, 4) || !aligned(out_logprob, 4))
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "misaligned beam_logprob or output pointer");
+  if (!workspace || workspace_bytes < need)
+    return fail(ADASERVE_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace ? workspace_bytes : (size_t)0,
+                need);
+  if (!aligned(workspace, 256)) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  const int32_t st = check_device();
+  if (st != ADASERVE_OK) return st;
+  BeamArgs a;
+  a.num_requests = num_requests;
+  a.beam_in = beam_in;
+  a.beam_out = beam_out;
+  a.rows = num_requests * beam_in;
+  a.vocab = vocab;
+  a.parts = parts;
+  a.row_stride = row_stride;
+  a.logits = logits;
+  a.beam_logprob = beam_logprob;
+  a.ws_ml = (float2 *)workspace;
+  a.ws_top = (uint64_t *)((char *)workspace + round_up((size_t)a.rows * parts * 8, 256));
+  a.out_parent = out_parent;
+  a.out_token = out_token;
+  a.out_logprob = out_logprob;
+  return launch_status(launch_beam_step(a, dtype == ADASERVE_BF16, (hipStream_t)stream), "beam step launch");
 }
 
 }  // extern "C"

@@ -105,4 +105,29 @@ struct SelectArgs {
 
 hipError_t launch_select_trees(const SelectArgs &a, hipStream_t stream);
 
+// One beam-search speculation step (beam.hip).
+constexpr int kBeamMaxWidth = 64;
+constexpr int kBeamMaxVocab = 1 << 20;
+constexpr int kBeamMaxParts = 32;   // row parts at kBeamMaxVocab (fp32: 32768 logits per part)
+
+struct BeamArgs {
+  int32_t num_requests;
+  int32_t beam_in;              // beams per request (rows per request)
+  int32_t beam_out;             // children kept per request
+  int32_t rows;                 // num_requests * beam_in
+  int32_t vocab;
+  int32_t parts;                // workgroups per row (beam_parts)
+  int64_t row_stride;           // elements between logit rows
+  const void *logits;           // [rows, row_stride]
+  const float *beam_logprob;    // [rows]
+  float2 *ws_ml;                // [rows, parts] (part max, sum of exp(x - max))
+  uint64_t *ws_top;             // [rows, parts, beam_out] sorted row keys (logit, token)
+  int32_t *out_parent;          // [num_requests, beam_out]
+  int32_t *out_token;
+  float *out_logprob;
+};
+
+int32_t beam_parts(int32_t vocab, bool bf16);
+hipError_t launch_beam_step(const BeamArgs &a, bool bf16, hipStream_t stream);
+
 }  // namespace adaserve

@@ -45,6 +45,10 @@ def kernel_kind(name: str) -> str:
         return "node_argmax"
     if "tree_accept" in name:
         return "tree_accept"
+    if "beam_scan" in name:
+        return "beam_scan"
+    if "beam_merge" in name:
+        return "beam_merge"
     return "other"
 
 

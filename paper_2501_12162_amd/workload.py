@@ -483,3 +483,60 @@ def make_candidates(rng: np.random.Generator, num_requests: int, depth: int, wid
                           cand_parent=np.concatenate(parents) if parents else np.zeros(0, np.int32),
                           cand_prob=np.concatenate(probs) if probs else np.zeros(0, np.float32),
                           need=need, budget=int(budget), n_max=int(n_max), depth=depth, width=width)
+
+
+# ---------------------------------------------------------------------------
+# Draft logits for one beam-search speculation step
+# ---------------------------------------------------------------------------
+
+@dataclass
+class BeamBatch:
+    """Inputs of one beam-search step (section 4.3 step 1): the draft model's
+    logits after every beam node, and each beam's log path probability.
+
+    logits: [num_requests * beam_in, row_stride] (bf16 bit patterns as
+    uint16, or float32); columns past ``vocab`` hold NaN.  beam_logprob:
+    [num_requests, beam_in] float32, natural-log path probabilities, best
+    beam first; -inf marks an unused beam slot.
+    """
+    logits: np.ndarray
+    beam_logprob: np.ndarray
+    vocab: int
+    dtype: str
+
+    @property
+    def num_requests(self) -> int:
+        return int(self.beam_logprob.shape[0])
+
+    @property
+    def beam_in(self) -> int:
+        return int(self.beam_logprob.shape[1])
+
+    def logits_f32(self) -> np.ndarray:
+        """[num_requests, beam_in, vocab] float32 view of the logit values."""
+        x = bf16_bits_to_f32(self.logits) if self.dtype == "bf16" else self.logits
+        return x[:, :self.vocab].reshape(self.num_requests, self.beam_in, self.vocab)
+
+
+def make_beam_batch(rng: np.random.Generator, num_requests: int, beam_in: int, vocab: int,
+                    dtype: str = "bf16", std: float = 2.0, row_pad: int = 0,
+                    root_step: bool = False, dead_beams: int = 0) -> BeamBatch:
+    """Draft logits ~ N(0, std) per row (rounded to bf16 for "bf16"); beam
+    log path probabilities are sorted cumulative sums of log U(0, 1] (the
+    shape a beam at depth > 1 has), or 0 for the root step.  `dead_beams`
+    trailing beam slots per request are marked unused (-inf)."""
+    rows = num_requests * beam_in
+    stride = vocab + row_pad
+    body = rng.standard_normal(size=(rows, stride), dtype=np.float32) * np.float32(std)
+    body[:, vocab:] = np.float32(np.nan)
+    logits = f32_to_bf16_bits(body) if dtype == "bf16" else body
+    if dtype == "bf16" and row_pad:
+        logits[:, vocab:] = BF16_NAN
+    if root_step:
+        lp = np.zeros((num_requests, beam_in), dtype=np.float32)
+    else:
+        steps = np.log(1.0 - rng.random((num_requests, beam_in, 3)))
+        lp = -np.sort(-steps.sum(axis=2), axis=1).astype(np.float32)
+    if dead_beams:
+        lp[:, beam_in - dead_beams:] = -np.inf
+    return BeamBatch(logits=logits, beam_logprob=lp, vocab=vocab, dtype=dtype)

@@ -200,3 +200,61 @@ def test_select_rejects_bad_arguments(lib, kw, code):
 
 def test_select_empty_batch_is_a_noop(lib):
     assert _select(lib, B=0, C=0, indptr=None, par=None, prob=None) == ada.ADASERVE_OK
+
+
+def _beam_ws(lib, B=2, w_in=4, V=1000, w_out=8, dtype=ada.ADASERVE_BF16):
+    return lib.adaserve_beam_step_workspace_bytes(B, w_in, V, w_out, dtype)
+
+
+def test_beam_workspace_query(lib):
+    # one scan part per 65536 bf16 (32768 fp32) logits of a row: a (max, sum)
+    # pair per part, 256-byte aligned, then w_out sorted entries per part
+    assert _beam_ws(lib, B=2, w_in=4, V=65536, w_out=8) == 256 + 2 * 4 * 1 * 8 * 8
+    assert _beam_ws(lib, B=2, w_in=4, V=65537, w_out=8) == 256 + 2 * 4 * 2 * 8 * 8
+    assert _beam_ws(lib, B=2, w_in=4, V=65536, w_out=8, dtype=ada.ADASERVE_F32) == 256 + 2 * 4 * 2 * 8 * 8
+    assert _beam_ws(lib, V=1 << 20) != SIZE_MAX
+    assert _beam_ws(lib, V=(1 << 20) + 1) == SIZE_MAX
+    assert _beam_ws(lib, B=0) == 0
+    assert _beam_ws(lib, w_in=0) == SIZE_MAX
+    assert _beam_ws(lib, w_in=65) == SIZE_MAX
+    assert _beam_ws(lib, w_out=65) == SIZE_MAX
+    assert _beam_ws(lib, V=0) == SIZE_MAX
+    assert _beam_ws(lib, dtype=7) == SIZE_MAX
+
+
+def _beam(lib, **kw):
+    args = dict(B=2, w_in=4, logits=0x1000 * 16, stride=1024, V=1000, dtype=ada.ADASERVE_BF16, lp=FAKE,
+                w_out=8, par=FAKE, tok=FAKE, out_lp=FAKE, ws=0x100000, ws_bytes=1 << 20)
+    args.update(kw)
+    return lib.adaserve_beam_step(args["B"], args["w_in"], args["logits"], args["stride"], args["V"],
+                                  args["dtype"], args["lp"], args["w_out"], args["par"], args["tok"],
+                                  args["out_lp"], args["ws"], args["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=-1), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(w_in=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(w_in=65), ada.ADASERVE_ERR_UNSUPPORTED),
+    (dict(w_out=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(w_out=65), ada.ADASERVE_ERR_UNSUPPORTED),
+    (dict(V=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(V=(1 << 20) + 8, stride=(1 << 20) + 8), ada.ADASERVE_ERR_UNSUPPORTED),
+    (dict(stride=999), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(stride=1001), ada.ADASERVE_ERR_INVALID_ARGUMENT),      # rows not 16-byte apart
+    (dict(logits=0x1000 * 16 + 2), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(dtype=3), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(logits=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(lp=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(out_lp=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(ws=None), ada.ADASERVE_ERR_WORKSPACE),
+    (dict(ws_bytes=64), ada.ADASERVE_ERR_WORKSPACE),
+    (dict(ws=0x100000 + 64), ada.ADASERVE_ERR_INVALID_ARGUMENT),  # workspace not 256-byte aligned
+])
+def test_beam_rejects_bad_arguments(lib, kw, code):
+    assert _beam(lib, **kw) == code
+    assert lib.adaserve_last_error()
+
+
+def test_beam_empty_batch_is_a_noop(lib):
+    assert _beam(lib, B=0, logits=None, lp=None, par=None, tok=None, out_lp=None, ws=None,
+                 ws_bytes=0) == ada.ADASERVE_OK
