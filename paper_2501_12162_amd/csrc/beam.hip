@@ -14,17 +14,21 @@
 //    chunk's best K = beam_out logits are then found without sorting the
 //    chunk: the K-th largest lane maximum T is a lower bound of the K-th
 //    largest logit (K lanes hold a value >= T), so every one of the best K
-//    is >= T.  T comes from a bitwise radix select on ballots (32 steps of
-//    one compare and a popcount); the logits >= T are gathered into LDS
-//    and, when at most 64, one per lane, K rounds of a wave maximum pick
-//    them in order.  More than 64 (ties at T, sorted rows) takes a general
+//    is >= T and sits in a "hot" lane (lane maximum >= T).  T comes from a
+//    bitwise radix select on ballots (32 steps of one compare and a
+//    popcount).  Hot lanes (usually K of them) copy their vectors to LDS,
+//    the whole wave filters them against T, and each of the (at most 64)
+//    survivors is placed by counting the survivors that beat it.  Many hot
+//    lanes or survivors (ties at T, sorted rows, wide beams) take a general
 //    path: a threshold-filtered LDS buffer cut back to its K best whenever
-//    it could overflow.  The workgroup then merges its waves' sorted lists
-//    and (max, sum) pairs.
-//  * beam_merge_kernel: one wave per request turns the parts' (max, sum)
-//    into lse per beam, adds log f(b) - lse to each part's sorted list (the
-//    offset is the same for a whole row, so row order by logit is row order
-//    by score) and merges the lists' heads in beam_out rounds.
+//    it could overflow.  The workgroup's list is the K best of its waves'
+//    lists, again placed by counting, plus the merged (max, sum).
+//  * beam_merge_kernel: one workgroup per request turns the parts' (max,
+//    sum) into lse per beam, adds log f(b) - lse to the parts' listed
+//    logits (the offset is the same for a whole row, so a row's best
+//    children by logit are its best by score), ranks each beam's candidates
+//    by counting, and merges the beams' sorted lists head by head in
+//    beam_out rounds of a wave maximum.
 //
 // Entries travel as 64-bit keys whose unsigned order is the ranking order
 // (see row_key and child_key), so every comparison is one integer compare
@@ -44,7 +48,11 @@ constexpr int kVecPerLane = 16;       // 16-byte vectors per lane per chunk
 constexpr int kScanWaves = 8;         // chunks (waves) per workgroup
 constexpr int kGather = 64;           // fast-path candidates per chunk
 constexpr int kCap = 640;             // general-path buffer entries per wave
-constexpr int kMergeEntries = 4096;   // request candidates staged in LDS by the merge
+constexpr int kStageLanes = 20;       // hot lanes staged in LDS (kStageLanes x 256 B fit the buffer)
+constexpr int kStageRounds = (kStageLanes * kVecPerLane + 63) / 64;
+static_assert(kStageLanes * kVecPerLane * 16 <= kCap * 8, "staged vectors must fit the per-wave buffer");
+constexpr int kMergeEntries = 4096;   // candidates staged in LDS by the merge
+constexpr int kMergeThreads = 256;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -162,12 +170,27 @@ __device__ int keep_best(uint64_t *buf, int count, int k, uint64_t &out) {
   return kept;
 }
 
+// Writes the K best of cand[0, n) (n <= 64, unique keys) to out[0, K) in
+// order, 0 past the n-th: each lane ranks one candidate by counting the
+// candidates that beat it.
+__device__ __forceinline__ void rank_into(const uint64_t *cand, int n, int K, uint64_t *out) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t c = lane < n ? cand[lane] : 0;
+  int rank = 0;
+  for (int j = 0; j < n; ++j) rank += cand[j] > c;
+  if (lane < n && rank < K) out[rank] = c;
+  if (lane >= n && lane < K) out[lane] = 0;
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(64 * kScanWaves) void beam_scan_kernel(BeamArgs a) {
   constexpr int EPV = BF16 ? 8 : 4;
   constexpr int ESZ = BF16 ? 2 : 4;
   constexpr int kChunk = 64 * kVecPerLane * EPV;
-  __shared__ uint64_t buf[kScanWaves][kCap];
+  __shared__ __attribute__((aligned(16))) uint64_t buf[kScanWaves][kCap];
+  __shared__ uint64_t lst[kScanWaves * kBeamMaxWidth];  // wave w's sorted list at [w * K, w * K + K)
+  __shared__ uint64_t cand[kScanWaves][kGather];
+  __shared__ int stage_lane[kScanWaves][kStageLanes];
   __shared__ int gathered[kScanWaves];
   __shared__ float wave_m[kScanWaves], wave_s[kScanWaves];
 
@@ -230,44 +253,64 @@ __global__ __launch_bounds__(64 * kScanWaves) void beam_scan_kernel(BeamArgs a) 
 #pragma unroll
     for (int v = 0; v < kVecPerLane; ++v) asm volatile("" : "+v"(w[v]));
 
-    // Threshold: the K-th largest lane maximum.
+    // Threshold: the K-th largest lane maximum.  Only "hot" lanes (maximum
+    // >= T) hold logits >= T; they copy their vectors to LDS, where the whole
+    // wave filters them.
     const float T = key_value(kth_largest_key(order_key(lane_m), K));
-    if (lane == 0) gathered[wave] = 0;
-    wave_sync_lds();
+    const bool hot = lane_m >= T && lane_m > -INFINITY;
+    const uint64_t hot_mask = __ballot(hot);
+    const int n_hot = __popcll(hot_mask);
+    int n_cand = kGather + 1;
+    if (n_hot <= kStageLanes) {
+      u32x4 *st = (u32x4 *)bw;
+      if (lane == 0) gathered[wave] = 0;
+      if (hot) {
+        const int slot = __popcll(hot_mask & ((1ull << lane) - 1));
 #pragma unroll
-    for (int v = 0; v < kVecPerLane; ++v) {
-      if (!__any(vmax[v] >= T && vmax[v] > -INFINITY)) continue;
-      const int e0 = first + (v * 64 + lane) * EPV;
+        for (int v = 0; v < kVecPerLane; ++v) st[slot * kVecPerLane + v] = w[v];
+        stage_lane[wave][slot] = lane;
+      }
+      wave_sync_lds();
+      const int n_vec = n_hot * kVecPerLane;
+      u32x4 sv[kStageRounds];
       int n = 0;
 #pragma unroll
-      for (int e = 0; e < EPV; ++e) {
-        const float x = elem<BF16>(w[v], e);
-        n += (x >= T && x > -INFINITY);
+      for (int i = 0; i < kStageRounds; ++i) {
+        const int q = lane + 64 * i;
+        if (q < n_vec) {
+          sv[i] = st[q];
+#pragma unroll
+          for (int e = 0; e < EPV; ++e) {
+            const float x = elem<BF16>(sv[i], e);
+            n += (x >= T && x > -INFINITY);
+          }
+        }
       }
       int slot = n ? atomicAdd(&gathered[wave], n) : 0;
 #pragma unroll
-      for (int e = 0; e < EPV; ++e) {
-        const float x = elem<BF16>(w[v], e);
-        if (x >= T && x > -INFINITY) {
-          if (slot < kGather) bw[slot] = row_key(x, e0 + e);
-          ++slot;
+      for (int i = 0; i < kStageRounds; ++i) {
+        const int q = lane + 64 * i;
+        if (q < n_vec) {
+          const int tok0 = first + ((q % kVecPerLane) * 64 + stage_lane[wave][q / kVecPerLane]) * EPV;
+#pragma unroll
+          for (int e = 0; e < EPV; ++e) {
+            const float x = elem<BF16>(sv[i], e);
+            if (x >= T && x > -INFINITY) {
+              if (slot < kGather) cand[wave][slot] = row_key(x, tok0 + e);
+              ++slot;
+            }
+          }
         }
       }
+      wave_sync_lds();
+      n_cand = gathered[wave];
+      if (n_cand <= kGather) rank_into(cand[wave], n_cand, K, lst + wave * K);
     }
-    wave_sync_lds();
-    const int n_cand = gathered[wave];
-    if (n_cand <= kGather) {
-      uint64_t c = lane < n_cand ? bw[lane] : 0;
-      for (int k = 0; k < K; ++k) {
-        const uint64_t m = wave_max_u64(c);
-        if (m == 0) break;
-        if (lane == k) mine = m;
-        if (c == m) c = 0;
-      }
-    } else {
-      // General path: filter against a rising threshold key; keys not below
-      // it are buffered, and the buffer is cut back to its K best before it
-      // could overflow.  Starts at the smallest key of value T.
+    if (n_cand > kGather) {
+      // General path (ties at T, sorted rows, wide beams): filter against a
+      // rising threshold key; keys not below it are buffered, and the buffer
+      // is cut back to its K best before it could overflow.  Starts at the
+      // smallest key of value T.
       uint64_t thr = (uint64_t)order_key(T) << 32;
       int count = 0;
       wave_sync_lds();
@@ -304,25 +347,43 @@ __global__ __launch_bounds__(64 * kScanWaves) void beam_scan_kernel(BeamArgs a) 
         count += __shfl(incl, 63, 64);
         wave_sync_lds();
       }
-      keep_best(bw, count, K, mine);
+      if (count <= kGather) {
+        rank_into(bw, count, K, lst + wave * K);
+      } else {
+        keep_best(bw, count, K, mine);
+        if (lane < K) lst[wave * K + lane] = mine;
+      }
     }
+  } else if (lane < K) {  // unused beam slot, or a chunk past the vocabulary
+    lst[wave * K + lane] = 0;
   }
 
-  // Wave results to LDS; the workgroup's (max, sum) and merged list.
+  // The workgroup's (max, sum) and its best K over the waves' lists, each
+  // list entry ranked against all of them.
   const float M = wave_max_f32(lane_m);
   float s = M > -INFINITY && lane_m > -INFINITY ? lane_s * __builtin_amdgcn_exp2f((lane_m - M) * kLog2e) : 0.f;
   s = wave_sum(s);
-  __syncthreads();  // every wave is done with its LDS buffer
   if (lane == 0) {
     wave_m[wave] = M;
     wave_s[wave] = s;
   }
-  if (lane < K) bw[lane] = mine;
   __syncthreads();
-  if (wave != 0) return;
-
   const int64_t unit = blockIdx.x;
-  if (lane == 0) {
+  const int t = threadIdx.x;
+  const int n = kScanWaves * K;
+  if (t < n) {
+    const uint64_t c = lst[t];
+    int rank = 0, nz = 0;
+    for (int j = 0; j < n; ++j) {
+      const uint64_t e = lst[j];
+      rank += e > c;
+      nz += e != 0;
+    }
+    uint64_t *top = a.ws_top + unit * K;
+    if (c != 0 && rank < K) top[rank] = c;
+    if (t < K && t >= nz) top[t] = 0;
+  }
+  if (t == 0) {
     float pm = -INFINITY;
     for (int w = 0; w < kScanWaves; ++w) pm = fmaxf(pm, wave_m[w]);
     float ps = 0.f;
@@ -331,35 +392,20 @@ __global__ __launch_bounds__(64 * kScanWaves) void beam_scan_kernel(BeamArgs a) 
         if (wave_m[w] > -INFINITY) ps += wave_s[w] * __builtin_amdgcn_exp2f((wave_m[w] - pm) * kLog2e);
     a.ws_ml[unit] = make_float2(pm, ps);
   }
-  // Head merge of the waves' sorted lists: lane l < kScanWaves follows list l.
-  uint64_t *top = a.ws_top + unit * K;
-  int head = 0;
-  uint64_t cur = lane < kScanWaves ? buf[lane][0] : 0;
-  int k = 0;
-  for (; k < K; ++k) {
-    const uint64_t m = wave_max_u64(cur);
-    if (m == 0) break;
-    if (lane == 0) top[k] = m;
-    if (lane < kScanWaves && cur == m) {
-      ++head;
-      cur = head < K ? buf[lane][head] : 0;
-    }
-  }
-  for (int j = k + lane; j < K; j += 64) top[j] = 0;
 }
 
-__global__ __launch_bounds__(64) void beam_merge_kernel(BeamArgs a) {
+__global__ __launch_bounds__(kMergeThreads) void beam_merge_kernel(BeamArgs a) {
   __shared__ float offset[kBeamMaxWidth];
-  __shared__ uint64_t staged[kMergeEntries];
-  __shared__ int heads[kBeamMaxWidth * kBeamMaxParts];
+  __shared__ uint64_t cand[kMergeEntries];                      // child keys of a batch of beams
+  __shared__ uint64_t blist[kBeamMaxWidth * kBeamMaxWidth];     // beam b's sorted list at [b * K, b * K + K)
   const int r = blockIdx.x;
-  const int lane = threadIdx.x;
+  const int t = threadIdx.x, lane = t & 63;
   const int W = a.beam_in, P = a.parts, K = a.beam_out;
-  const int lists = W * P;
-  const uint64_t *top = a.ws_top + (int64_t)r * lists * K;
+  const int per_beam = P * K;
+  const uint64_t *top = a.ws_top + (int64_t)r * W * per_beam;
 
   // log f(b) - lse(row b) per beam, from the row's parts.
-  for (int b = lane; b < W; b += 64) {
+  for (int b = t; b < W; b += kMergeThreads) {
     const int row = r * W + b;
     const float2 *ml = a.ws_ml + (int64_t)row * P;
     float m = -INFINITY;
@@ -371,50 +417,64 @@ __global__ __launch_bounds__(64) void beam_merge_kernel(BeamArgs a) {
     const float lp = a.beam_logprob[row];
     offset[b] = (lp > -INFINITY && m > -INFINITY) ? lp - (m + log2f(s) * kLn2) : -INFINITY;
   }
-  const bool staged_all = lists * K <= kMergeEntries;
-  if (staged_all)
-    for (int j = lane; j < lists * K; j += 64) staged[j] = top[j];
-  for (int l = lane; l < lists; l += 64) heads[l] = 0;
   __syncthreads();
 
-  // Ranking key of list l's current head (0: list exhausted or no child).
-  auto head_key = [&](int l) -> uint64_t {
-    const int h = heads[l];
-    if (h >= K) return 0;
-    const uint64_t e = staged_all ? staged[l * K + h] : top[(int64_t)l * K + h];
-    if (e == 0) return 0;
-    const float x = row_key_value(e);
-    const int b = l / P;
-    const float score = offset[b] + x;
-    if (!(x > -INFINITY) || !(score > -INFINITY)) return 0;
-    return child_key(score, b, row_key_token(e));
-  };
-  int kept = 0;
-  for (int k = 0; k < K; ++k) {
-    uint64_t best = 0;
-    int best_l = -1;
-    for (int l = lane; l < lists; l += 64) {
-      const uint64_t c = head_key(l);
-      if (c > best) {
-        best = c;
-        best_l = l;
+  // Each beam's best K children, ranked among its parts' lists, in batches
+  // of beams whose candidates fit in LDS.
+  const int batch = kMergeEntries / per_beam;  // >= 1: per_beam <= kBeamMaxParts * kBeamMaxWidth
+  for (int b0 = 0; b0 < W; b0 += batch) {
+    const int n = min(batch, W - b0) * per_beam;
+    for (int c = t; c < n; c += kMergeThreads) {
+      const int b = b0 + c / per_beam;
+      const uint64_t e = top[(int64_t)b0 * per_beam + c];
+      uint64_t key = 0;
+      if (e != 0) {
+        const float x = row_key_value(e);
+        const float score = offset[b] + x;
+        if (x > -INFINITY && score > -INFINITY) key = child_key(score, b, row_key_token(e));
       }
+      cand[c] = key;
     }
-    const uint64_t m = wave_max_u64(best);
+    __syncthreads();
+    for (int c = t; c < n; c += kMergeThreads) {
+      const int base = c / per_beam * per_beam;
+      const uint64_t key = cand[c];
+      int rank = 0, nz = 0;
+      for (int j = 0; j < per_beam; ++j) {
+        const uint64_t e = cand[base + j];
+        rank += e > key;
+        nz += e != 0;
+      }
+      const int b = b0 + c / per_beam;
+      if (key != 0 && rank < K) blist[b * K + rank] = key;
+      const int pos = c - base;
+      if (pos < K && pos >= nz) blist[b * K + pos] = 0;
+    }
+    __syncthreads();
+  }
+
+  // Head merge across the beams' sorted lists: lane b follows beam b.
+  if (t >= 64) return;
+  int head = 0;
+  uint64_t cur = lane < W ? blist[lane * K] : 0;
+  int k = 0;
+  for (; k < K; ++k) {
+    const uint64_t m = wave_max_u64(cur);
     if (m == 0) break;  // fewer children than slots
-    if (best == m) ++heads[best_l];
     if (lane == 0) {
       a.out_parent[r * K + k] = 63 - (int)((m >> 20) & 63);
       a.out_token[r * K + k] = 0xfffff - (int)(m & 0xfffff);
       a.out_logprob[r * K + k] = key_value((uint32_t)(m >> 32));
     }
-    ++kept;
-    wave_sync_lds();
+    if (lane < W && cur == m) {
+      ++head;
+      cur = head < K ? blist[lane * K + head] : 0;
+    }
   }
-  for (int k = kept + lane; k < K; k += 64) {
-    a.out_parent[r * K + k] = -1;
-    a.out_token[r * K + k] = -1;
-    a.out_logprob[r * K + k] = -INFINITY;
+  for (int j = k + lane; j < K; j += 64) {
+    a.out_parent[r * K + j] = -1;
+    a.out_token[r * K + j] = -1;
+    a.out_logprob[r * K + j] = -INFINITY;
   }
 }
 
@@ -434,7 +494,7 @@ hipError_t launch_beam_step(const BeamArgs &a, bool bf16, hipStream_t stream) {
     hipLaunchKernelGGL(beam_scan_kernel<false>, dim3(blocks), dim3(64 * kScanWaves), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(beam_merge_kernel, dim3((unsigned)a.num_requests), dim3(64), 0, stream, a);
+  hipLaunchKernelGGL(beam_merge_kernel, dim3((unsigned)a.num_requests), dim3(kMergeThreads), 0, stream, a);
   return hipGetLastError();
 }
 
