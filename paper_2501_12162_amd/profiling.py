@@ -26,13 +26,31 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CALIB_BYTES = 256 << 20
 
 
+_TRAFFIC_FILES = ("tree_attn.hip", "argmax.hip", "plan.h", "device_common.h")
+
+
+def _block(text: str, start: str, end: str) -> str:
+    i = text.index(start)
+    return text[i:text.index(end, i)]
+
+
 def kernel_source_hash() -> str:
-    """sha256 over the HIP/C++ sources and internal headers of the library."""
+    """sha256 over the sources that decide the measured kernels' traffic: the
+    tree-attention and argmax kernels, their headers, the attention argument
+    block and the host planner and launch path (other entry points do not
+    change it)."""
     h = hashlib.sha256()
-    for p in sorted(glob.glob(os.path.join(PKG, "csrc", "*"))):
-        with open(p, "rb") as f:
-            h.update(os.path.basename(p).encode())
+    csrc = os.path.join(PKG, "csrc")
+    for name in _TRAFFIC_FILES:
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode())
             h.update(f.read())
+    with open(os.path.join(csrc, "kernels.h")) as f:
+        h.update(_block(f.read(), "struct TreeAttnArgs", "};").encode())
+    with open(os.path.join(csrc, "adaserve.cpp")) as f:
+        text = f.read()
+    h.update(_block(text, "struct AttnShape", "// Beam step:").encode())
+    h.update(_block(text, "int32_t adaserve_tree_attn_verify(", "int32_t adaserve_tree_accept(").encode())
     return h.hexdigest()[:16]
 
 
