@@ -188,3 +188,68 @@ def test_repeated_calls_reuse_the_workspace(torch_cuda):
     three = _run(torch_cuda, b.logits, b.vocab, b.beam_logprob, 8, "bf16", calls=3)
     for a, c in zip(one, three):
         np.testing.assert_array_equal(a, c)
+
+
+def test_chained_steps_replayed_from_a_graph(torch_cuda):
+    """d speculation steps (the first from the roots, each later one taking
+    the previous step's kept children as its beams) captured once in a HIP
+    graph and replayed, as the draft steps after the first are replayed from
+    a captured graph (section 5.2).  Every replay must reproduce the eager
+    chain exactly; eager work runs between replays."""
+    import paper_2501_12162_amd as ada
+    torch = torch_cuda
+    rng = np.random.Generator(np.random.PCG64(11))
+    B, w, V, d = 6, 4, 30000, 4
+    dev = torch.device("cuda")
+    logits = []
+    for k in range(d):
+        b = make_beam_batch(rng, B, 1 if k == 0 else w, V)
+        logits.append(torch.from_numpy(b.logits.view(np.int16)).to(dev).view(torch.bfloat16))
+    root_lp = torch.zeros(B, 1, dtype=torch.float32, device=dev)
+    outs = [(torch.empty(B, w, dtype=torch.int32, device=dev), torch.empty(B, w, dtype=torch.int32, device=dev),
+             torch.empty(B, w, dtype=torch.float32, device=dev)) for _ in range(d)]
+    nbytes = max(ada.adaserve_beam_step_workspace_bytes(B, 1 if k == 0 else w, V, w, ada.ADASERVE_BF16)
+                 for k in range(d))
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+
+    def chain():
+        lp = root_lp
+        for k in range(d):
+            par, tok, out = outs[k]
+            ada.adaserve_beam_step(logits=logits[k], vocab=V, beam_logprob=lp, out_parent=par, out_token=tok,
+                                   out_logprob=out, workspace=ws)
+            lp = out
+
+    chain()
+    torch.cuda.synchronize()
+    eager = [[t.clone() for t in o] for o in outs]
+    # the eager chain agrees with the oracle step by step
+    lp = np.zeros((B, 1))
+    for k in range(d):
+        x = bf16_bits_to_f32(logits[k].view(torch.int16).cpu().numpy().view(np.uint16)).astype(np.float64)
+        x = x.reshape(B, lp.shape[1], V)
+        opar, otok, olp = oracle.beam_step(logits=x, beam_logprob=lp, w_out=w)
+        got_lp = eager[k][2].cpu().numpy()
+        np.testing.assert_allclose(got_lp, olp, rtol=0, atol=SCORE_TOL * 4)
+        lp = got_lp.astype(np.float64)   # next step from the kernel's own scores
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        chain()   # warm-up on the side stream before capture
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        chain()
+    for rep in range(4):
+        for o in outs:
+            for t in o:
+                t.fill_(-5)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k in range(d):
+            for a_, b_ in zip(outs[k], eager[k]):
+                assert torch.equal(a_, b_), (rep, k)
+        chain()   # eager work between replays
+        torch.cuda.synchronize()
