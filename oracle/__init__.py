@@ -369,3 +369,110 @@ def beam_step(*, logits, beam_logprob, w_out: int):
         token[r, :k] = tt.ravel()[order]
         out[r, :k] = s[order]
     return parent, token, out
+
+
+def _sampled_tree_ok(par, n):
+    if n < 1 or n > 128 or par[0] != -1:
+        return False
+    return all(0 <= par[i] < i for i in range(1, n))
+
+
+def tree_accept_sampled(*, node_indptr, parent, draft_tokens, target_logits, draft_logits, vocab: int,
+                        u_accept, u_bonus, max_accept: int):
+    """Tree verification for sampled decoding: multi-step speculative
+    sampling over the draft token tree (section 4.3 step 4 delegates
+    verification to tree-based prior work; the reading here is the
+    token-tree form of speculative sampling, lossless when each node's
+    children were drawn independently from the draft distribution at that
+    node).
+
+    Row u of target_logits / draft_logits holds the target / draft model's
+    logits after node u's root path (already divided by the sampling
+    temperature); softmax gives p_u and q_u.  From the root: the children of
+    the current node u are tried in index order; child c with token t is
+    accepted when u_accept[c] * q_u(t) < p_res(t), i.e. with probability
+    min(1, p_res(t) / q_u(t)); after a rejection p_res becomes
+    max(0, p_res - q_u), renormalised.  An accepted child becomes the current
+    node (its token is emitted); when no child is accepted (or u is a leaf)
+    the bonus token is drawn from p_res by inverse CDF: the smallest v whose
+    cumulative probability exceeds u_bonus[u], and the walk ends.  p_res
+    starts as p_u at every node.  A rejection that leaves p_res without mass
+    (possible only through rounding) ends the walk with the bonus drawn from
+    p_res before it.
+
+    Outputs follow tree_accept: accept_len = accepted drafts + 1, accept_nodes
+    = the path from the root, accept_tokens = the accepted drafts' tokens then
+    the bonus token; -1 for a malformed tree (as tree_accept), a draft token
+    of a non-root node outside [0, vocab), or a tree deeper than
+    max_accept - 1.  Also returns, per request, the smallest relative margin
+    of any decision taken (acceptance test or CDF boundary), so callers
+    comparing against float32 arithmetic can tell decisive cases from near
+    ties.  float64 throughout.
+    """
+    indptr = np.asarray(node_indptr, dtype=np.int64)
+    par_all = np.asarray(parent, dtype=np.int64)
+    draft = np.asarray(draft_tokens, dtype=np.int64)
+    ua = np.asarray(u_accept, dtype=np.float64)
+    ub = np.asarray(u_bonus, dtype=np.float64)
+    B = indptr.size - 1
+    alen = np.full(B, -1, np.int32)
+    tok = np.full((B, max_accept), -1, np.int32)
+    nodes = np.full((B, max_accept), -1, np.int32)
+    margin = np.full(B, np.inf)
+
+    def softmax(row):
+        x = np.asarray(row[:vocab], dtype=np.float64)
+        e = np.exp(x - x.max())
+        return e / e.sum()
+
+    def draw(res, u):
+        cdf = np.cumsum(res)
+        v = int(np.searchsorted(cdf, u, side="right"))
+        last = int(np.nonzero(res > 0)[0][-1])
+        v = min(v, last)
+        lo = cdf[v - 1] if v > 0 else 0.0
+        return v, min(abs(cdf[v] - u), abs(u - lo))
+
+    for r in range(B):
+        base, n = int(indptr[r]), int(indptr[r + 1] - indptr[r])
+        par = par_all[base:base + n]
+        if not _sampled_tree_ok(par, n):
+            continue
+        depth = np.zeros(n, np.int64)
+        for i in range(1, n):
+            depth[i] = depth[par[i]] + 1
+        if depth.max() > max_accept - 1 or any(not (0 <= draft[base + i] < vocab) for i in range(1, n)):
+            continue
+        u, path, out, m = 0, [0], [], np.inf
+        while True:
+            p = softmax(target_logits[base + u])
+            children = [i for i in range(u + 1, n) if par[i] == u]
+            res = p
+            nxt = None
+            if children:
+                q = softmax(draft_logits[base + u])
+                for c in children:
+                    t = int(draft[base + c])
+                    lhs, rhs = ua[base + c] * q[t], res[t]
+                    m = min(m, abs(rhs - lhs) / max(rhs, lhs, 1e-300))
+                    if lhs < rhs:
+                        nxt = c
+                        break
+                    left = np.maximum(res - q, 0.0)
+                    if left.sum() <= 0.0:
+                        break
+                    res = left / left.sum()
+            if nxt is None:
+                v, gap = draw(res, ub[base + u])
+                m = min(m, gap)
+                out.append(v)
+                break
+            out.append(int(draft[base + nxt]))
+            path.append(nxt)
+            u = nxt
+        k = len(path)
+        alen[r] = k
+        nodes[r, :k] = path
+        tok[r, :k] = out
+        margin[r] = m
+    return alen, tok, nodes, margin
