@@ -300,6 +300,39 @@ def main():
     torch.cuda.synchronize()
     beam_us = commit_ev[0].elapsed_time(commit_ev[1]) * 1e3 / 20
 
+    # Sampled-decoding verification of the same batch (the stochastic
+    # counterpart of argmax + acceptance; not part of the timed greedy step):
+    # draft logits a noisy copy of the target's, one uniform per node for the
+    # acceptance test and one for the bonus draw.
+    from paper_2501_12162_amd.workload import make_draft_logits, make_uniforms
+    srng = np.random.Generator(np.random.PCG64(200 + args.workload))
+    dl = make_draft_logits(srng, b.logits, b.vocab, b.dtype, 0.5)
+    d_logits = torch.from_numpy(dl.view(np.int16) if is_bf16_in(b) else dl).cuda()
+    if is_bf16_in(b):
+        d_logits = d_logits.view(torch.bfloat16)
+    del dl
+    u_acc = tdev(make_uniforms(srng, b.total_nodes))
+    u_bon = tdev(make_uniforms(srng, b.total_nodes))
+    s_len = torch.empty_like(dev.accept_len)
+    s_tok = torch.empty_like(dev.accept_tokens)
+    s_nodes = torch.empty_like(dev.accept_nodes)
+
+    def sampled():
+        ada.adaserve_tree_accept_sampled(node_indptr=dev.node_indptr, parent=dev.parent, draft_tokens=dev.draft_tokens,
+                                         target_logits=rp["logits"], draft_logits=d_logits, vocab=b.vocab,
+                                         u_accept=u_acc, u_bonus=u_bon, max_accept=dev.max_accept, accept_len=s_len,
+                                         accept_tokens=s_tok, accept_nodes=s_nodes)
+    sampled()
+    torch.cuda.synchronize()
+    calib_dst.copy_(calib_src)
+    commit_ev[0].record(stream)
+    for _ in range(10):
+        sampled()
+    commit_ev[1].record(stream)
+    torch.cuda.synchronize()
+    sampled_us = commit_ev[0].elapsed_time(commit_ev[1]) * 1e3 / 10
+    sampled_len = s_len.cpu().numpy()
+
     attn_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
     argmax_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
     accept_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
@@ -370,6 +403,8 @@ def main():
             "kv_commit_bytes": committed_rows * 4 * b.num_kv_heads * b.head_dim * (2 if is_bf16 else 4),
             "select_us": select_us,
             "select_candidates": int(cands.cand_prob.size),
+            "sampled_accept_us": sampled_us,
+            "sampled_accepted_tokens": int(sampled_len.sum()),
             "beam_step_us": beam_us,
             "beam_step_rows": int(bb.logits.shape[0]),
             "beam_step_hbm_frac": beam_bytes / (beam_us * 1e-6) / 1e9 / HBM_PEAK_GBS,

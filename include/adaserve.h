@@ -14,6 +14,8 @@
  *   adaserve_node_argmax       the target's greedy choice at every node;
  *   adaserve_tree_accept       the longest accepted root path per request and
  *                              the tokens it commits;
+ *   adaserve_tree_accept_sampled  the same for sampled decoding (speculative
+ *                              sampling over the tree);
  *   adaserve_commit_accepted_kv  the accepted path's keys and values written
  *                              into the request's paged cache;
  *   adaserve_select_trees      (before the pass) the two selection phases that
@@ -288,6 +290,47 @@ int32_t adaserve_beam_step(int32_t num_requests, int32_t beam_in, const void *lo
                            const float *beam_logprob, int32_t beam_out, int32_t *out_parent,
                            int32_t *out_token, float *out_logprob, void *workspace,
                            size_t workspace_bytes, void *stream);
+
+/*
+ * Tree verification for sampled decoding: multi-step speculative sampling
+ * over each request's draft token tree (the tree-based verification of prior
+ * work that section 4.3 step 4 delegates to; lossless -- the emitted tokens
+ * follow the target distribution -- when each node's children were drawn
+ * independently from the draft distribution at that node).  The greedy
+ * counterpart is adaserve_tree_accept.
+ *
+ * Row u of target_logits / draft_logits ([total_nodes, row_stride], dtype)
+ * holds the target / draft model's logits after node u's root path, already
+ * divided by the sampling temperature; p_u / q_u are their softmax over
+ * columns 0 .. vocab - 1.  Draft rows of leaves are never read.  From the
+ * root, the children of the current node u are tried in index order: child
+ * c with token t = draft_tokens[c] is accepted when
+ *   u_accept[c] * q_u(t) < p_res(t)
+ * (probability min(1, p_res(t) / q_u(t)) for u_accept uniform in [0, 1)),
+ * where p_res starts as p_u at every node; a rejection replaces p_res by
+ * max(0, p_res - q_u), renormalised.  The accepted child becomes the current
+ * node and its token is emitted; when no child is accepted (or u is a leaf)
+ * the bonus token -- the smallest v whose cumulative p_res, in token order,
+ * exceeds u_bonus[u] -- is emitted and the walk ends.  A rejection that
+ * leaves p_res without mass (possible only through rounding) ends the walk
+ * with the bonus drawn from p_res before it.  Arithmetic is fp32.
+ *
+ * Outputs as adaserve_tree_accept: accept_len[r] = accepted drafts + 1,
+ * accept_nodes[r] = the path from the root, accept_tokens[r] = the accepted
+ * drafts' tokens then the bonus token, -1 past them; accept_len = -1 and rows
+ * of -1 for a malformed tree (as adaserve_tree_accept), a draft token of a
+ * non-root node outside [0, vocab), or a tree deeper than max_accept - 1.
+ * u_accept, u_bonus: [total_nodes] fp32 (device).  Logits 16-byte aligned,
+ * row_stride * element size a multiple of 16 bytes.  One workgroup walks one
+ * request; requests run in parallel.
+ */
+int32_t adaserve_tree_accept_sampled(int32_t num_requests, int32_t total_nodes,
+                                     const int32_t *node_indptr, const int32_t *parent,
+                                     const int32_t *draft_tokens, const void *target_logits,
+                                     const void *draft_logits, int64_t row_stride, int32_t vocab,
+                                     int32_t dtype, const float *u_accept, const float *u_bonus,
+                                     int32_t max_accept, int32_t *accept_len,
+                                     int32_t *accept_tokens, int32_t *accept_nodes, void *stream);
 
 /* Message describing the last non-OK status returned on this thread. */
 const char *adaserve_last_error(void);

@@ -404,10 +404,10 @@ def tree_accept_sampled(*, node_indptr, parent, draft_tokens, target_logits, dra
     = the path from the root, accept_tokens = the accepted drafts' tokens then
     the bonus token; -1 for a malformed tree (as tree_accept), a draft token
     of a non-root node outside [0, vocab), or a tree deeper than
-    max_accept - 1.  Also returns, per request, the smallest relative margin
-    of any decision taken (acceptance test or CDF boundary), so callers
-    comparing against float32 arithmetic can tell decisive cases from near
-    ties.  float64 throughout.
+    max_accept - 1.  For callers comparing against float32 arithmetic, also
+    returns per request the smallest relative margin of its acceptance tests
+    (inf when it took none) and the cumulative distribution the bonus token
+    was drawn from (None for a malformed request).  float64 throughout.
     """
     indptr = np.asarray(node_indptr, dtype=np.int64)
     par_all = np.asarray(parent, dtype=np.int64)
@@ -419,6 +419,7 @@ def tree_accept_sampled(*, node_indptr, parent, draft_tokens, target_logits, dra
     tok = np.full((B, max_accept), -1, np.int32)
     nodes = np.full((B, max_accept), -1, np.int32)
     margin = np.full(B, np.inf)
+    bonus_cdf = [None] * B
 
     def softmax(row):
         x = np.asarray(row[:vocab], dtype=np.float64)
@@ -429,9 +430,7 @@ def tree_accept_sampled(*, node_indptr, parent, draft_tokens, target_logits, dra
         cdf = np.cumsum(res)
         v = int(np.searchsorted(cdf, u, side="right"))
         last = int(np.nonzero(res > 0)[0][-1])
-        v = min(v, last)
-        lo = cdf[v - 1] if v > 0 else 0.0
-        return v, min(abs(cdf[v] - u), abs(u - lo))
+        return min(v, last), cdf
 
     for r in range(B):
         base, n = int(indptr[r]), int(indptr[r + 1] - indptr[r])
@@ -463,8 +462,8 @@ def tree_accept_sampled(*, node_indptr, parent, draft_tokens, target_logits, dra
                         break
                     res = left / left.sum()
             if nxt is None:
-                v, gap = draw(res, ub[base + u])
-                m = min(m, gap)
+                v, cdf = draw(res, ub[base + u])
+                bonus_cdf[r] = cdf
                 out.append(v)
                 break
             out.append(int(draft[base + nxt]))
@@ -475,4 +474,4 @@ def tree_accept_sampled(*, node_indptr, parent, draft_tokens, target_logits, dra
         nodes[r, :k] = path
         tok[r, :k] = out
         margin[r] = m
-    return alen, tok, nodes, margin
+    return alen, tok, nodes, margin, bonus_cdf

@@ -41,6 +41,8 @@ SIGNATURES = {
     "adaserve_select_trees": (_I32, [_I32, _I32, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P]),
     "adaserve_beam_step_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, _I32]),
     "adaserve_beam_step": (_I32, [_I32, _I32, _P, _I64, _I32, _I32, _P, _I32, _P, _P, _P, _P, _SZ, _P]),
+    "adaserve_tree_accept_sampled": (_I32, [_I32, _I32, _P, _P, _P, _P, _P, _I64, _I32, _I32, _P, _P, _I32,
+                                            _P, _P, _P, _P]),
     "adaserve_last_error": (ctypes.c_char_p, []),
 }
 
@@ -211,4 +213,21 @@ def adaserve_beam_step(*, logits, vocab: int, beam_logprob, out_parent, out_toke
         int(B), int(w_in), _dptr(logits), int(stride), int(vocab), _dtype_code(logits), _dptr(beam_logprob),
         int(out_parent.shape[1]), _dptr(out_parent), _dptr(out_token), _dptr(out_logprob), _dptr(workspace),
         int(ws_bytes), _stream(stream))
+    _check(st)
+
+
+def adaserve_tree_accept_sampled(*, node_indptr, parent, draft_tokens, target_logits, draft_logits, vocab: int,
+                                 u_accept, u_bonus, max_accept: int, accept_len, accept_tokens, accept_nodes,
+                                 stream=None) -> None:
+    """Sampled-decoding tree verification; logits [T, row_stride] (temperature applied),
+    u_accept / u_bonus [T] float32; outputs as adaserve_tree_accept."""
+    B = node_indptr.shape[0] - 1
+    T, stride = target_logits.shape
+    if draft_logits.shape != target_logits.shape or draft_logits.dtype != target_logits.dtype:
+        raise ValueError("draft_logits must match target_logits in shape and dtype")
+    st = load_library().adaserve_tree_accept_sampled(
+        int(B), int(parent.shape[0]), _dptr(node_indptr), _dptr(parent), _dptr(draft_tokens),
+        _dptr(target_logits), _dptr(draft_logits), int(stride), int(vocab), _dtype_code(target_logits),
+        _dptr(u_accept), _dptr(u_bonus), int(max_accept), _dptr(accept_len), _dptr(accept_tokens),
+        _dptr(accept_nodes), _stream(stream))
     _check(st)

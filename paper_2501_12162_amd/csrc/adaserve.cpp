@@ -617,4 +617,50 @@ int32_t adaserve_beam_step(int32_t num_requests, int32_t beam_in, const void *lo
   return launch_status(launch_beam_step(a, dtype == ADASERVE_BF16, (hipStream_t)stream), "beam step launch");
 }
 
+int32_t adaserve_tree_accept_sampled(int32_t num_requests, int32_t total_nodes, const int32_t *node_indptr,
+                                     const int32_t *parent, const int32_t *draft_tokens, const void *target_logits,
+                                     const void *draft_logits, int64_t row_stride, int32_t vocab, int32_t dtype,
+                                     const float *u_accept, const float *u_bonus, int32_t max_accept,
+                                     int32_t *accept_len, int32_t *accept_tokens, int32_t *accept_nodes,
+                                     void *stream) {
+  if (num_requests < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_requests %d < 0", num_requests);
+  if (total_nodes < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "total_nodes %d < 0", total_nodes);
+  if (max_accept < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "max_accept %d < 1", max_accept);
+  if (vocab < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "vocab %d < 1", vocab);
+  if (row_stride < vocab)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "row_stride %lld < vocab %d", (long long)row_stride, vocab);
+  if (dtype != ADASERVE_F32 && dtype != ADASERVE_BF16)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "dtype %d is neither F32 nor BF16", dtype);
+  if ((int64_t)num_requests * max_accept > INT32_MAX)
+    return fail(ADASERVE_ERR_UNSUPPORTED, "num_requests * max_accept exceeds 2^31 - 1");
+  if (num_requests == 0) return ADASERVE_OK;
+  if (!node_indptr || !accept_len || !accept_tokens || !accept_nodes)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  if (total_nodes > 0 && (!parent || !draft_tokens || !target_logits || !draft_logits || !u_accept || !u_bonus))
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  const int64_t esz = dtype == ADASERVE_BF16 ? 2 : 4;
+  if (!aligned(target_logits, 16) || !aligned(draft_logits, 16) || (row_stride * esz) % 16 != 0)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT,
+                "logits must be 16-byte aligned with rows a multiple of 16 bytes apart");
+  const int32_t st = check_device();
+  if (st != ADASERVE_OK) return st;
+  SampledArgs a;
+  a.num_requests = num_requests;
+  a.total_nodes = total_nodes;
+  a.node_indptr = node_indptr;
+  a.parent = parent;
+  a.draft_tokens = draft_tokens;
+  a.target_logits = target_logits;
+  a.draft_logits = draft_logits;
+  a.row_stride = row_stride;
+  a.vocab = vocab;
+  a.u_accept = u_accept;
+  a.u_bonus = u_bonus;
+  a.max_accept = max_accept;
+  a.accept_len = accept_len;
+  a.accept_tokens = accept_tokens;
+  a.accept_nodes = accept_nodes;
+  return launch_status(launch_sampled_accept(a, dtype == ADASERVE_BF16, (hipStream_t)stream), "sampled accept launch");
+}
+
 }  // extern "C"

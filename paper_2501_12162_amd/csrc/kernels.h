@@ -130,4 +130,27 @@ struct BeamArgs {
 int32_t beam_parts(int32_t vocab, bool bf16);
 hipError_t launch_beam_step(const BeamArgs &a, bool bf16, hipStream_t stream);
 
+// Tree verification for sampled decoding (sampled.hip).
+constexpr int kMaxSampledNodes = 128;
+
+struct SampledArgs {
+  int32_t num_requests;
+  int32_t total_nodes;
+  const int32_t *node_indptr;   // [B + 1]
+  const int32_t *parent;        // [T] local ids
+  const int32_t *draft_tokens;  // [T]
+  const void *target_logits;    // [T, row_stride]
+  const void *draft_logits;     // [T, row_stride]
+  int64_t row_stride;           // elements
+  int32_t vocab;
+  const float *u_accept;        // [T]
+  const float *u_bonus;         // [T]
+  int32_t max_accept;
+  int32_t *accept_len;          // [B]
+  int32_t *accept_tokens;       // [B, max_accept]
+  int32_t *accept_nodes;        // [B, max_accept]
+};
+
+hipError_t launch_sampled_accept(const SampledArgs &a, bool bf16, hipStream_t stream);
+
 }  // namespace adaserve

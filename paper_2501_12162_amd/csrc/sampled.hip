@@ -1,0 +1,331 @@
+// Tree verification for sampled decoding on gfx950: multi-step speculative
+// sampling over each request's draft token tree (the tree-based verification
+// of prior work that section 4.3 step 4 delegates to).
+//
+// From the root, the children of the current node u are tried in index
+// order; child c with token t is accepted when u_accept[c] * q_u(t) <
+// p_res(t), p_u / q_u being the target / draft softmax at u and p_res
+// starting as p_u; a rejection replaces p_res by max(0, p_res - q_u),
+// renormalised.  An accepted child becomes the current node; otherwise the
+// bonus token is drawn from p_res (inverse CDF at u_bonus[u]) and the walk
+// ends.
+//
+// Every residual has the closed form max(0, p - c q) / S: after a
+// rejection c grows by the previous S and S is the new residual's mass
+// (if p_res = r/S with r = max(0, p - c q), then max(0, p_res - q) is
+// proportional to max(0, p - (c + S) q)).  So a node costs one pass over its
+// two logits rows for the softmax statistics, one more pass per rejection
+// (the new S), and the bonus draw two passes (segment sums, then a scan of
+// the one segment that holds the target).  One workgroup of 1024 threads
+// walks one request; the walk is sequential, requests run side by side.
+#include <limits.h>
+
+#include "device_common.h"
+#include "kernels.h"
+
+namespace adaserve {
+
+namespace {
+
+constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / 64;
+constexpr float kLog2e = 1.4426950408889634f;
+
+template <bool BF16>
+__device__ __forceinline__ float elem(const u32x4 &w, int e) {
+  if (BF16) return __uint_as_float((e & 1) ? (w[e >> 1] & 0xffff0000u) : (w[e >> 1] << 16));
+  return __uint_as_float(w[e]);
+}
+
+template <bool BF16>
+__device__ __forceinline__ float load_one(const void *row, int v) {
+  if (BF16) return bf16_bits_to_float(((const uint16_t *)row)[v]);
+  return ((const float *)row)[v];
+}
+
+struct Shared {
+  int32_t parent[kMaxSampledNodes];
+  int32_t token[kMaxSampledNodes];
+  int32_t depth[kMaxSampledNodes];
+  int32_t path[kMaxSampledNodes];
+  int32_t out[kMaxSampledNodes];
+  float red_a[kWaves];
+  float red_b[kWaves];
+  float scan[kThreads];
+  int32_t bad;
+  int32_t pick;
+};
+
+// Block-wide sum (every thread gets it).
+__device__ float block_sum(float v, Shared &sh) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) sh.red_a[wave] = v;
+  __syncthreads();
+  float t = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) t += sh.red_a[w];
+  __syncthreads();
+  return t;
+}
+
+// Block-wide (max, sum of exp(x - max)) merge of per-thread pairs.
+__device__ void block_max_sum(float &m, float &s, Shared &sh) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float wm = m;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) wm = fmaxf(wm, __shfl_xor(wm, off, 64));
+  float ws = wm > -INFINITY && m > -INFINITY ? s * exp2f((m - wm) * kLog2e) : 0.f;
+  ws = wave_sum(ws);
+  if (lane == 0) {
+    sh.red_a[wave] = wm;
+    sh.red_b[wave] = ws;
+  }
+  __syncthreads();
+  float M = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sh.red_a[w]);
+  float S = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w)
+    if (sh.red_a[w] > -INFINITY) S += sh.red_b[w] * exp2f((sh.red_a[w] - M) * kLog2e);
+  __syncthreads();
+  m = M;
+  s = S;
+}
+
+// Softmax statistics (max, sum of exp(x - max)) of one logits row.
+template <bool BF16>
+__device__ void row_stats(const char *row, int vocab, float &M, float &S, Shared &sh) {
+  constexpr int EPV = BF16 ? 8 : 4;
+  const int nvec = vocab / EPV;
+  float m = -INFINITY, s = 0.f;
+  for (int i = threadIdx.x; i < nvec; i += kThreads) {
+    const u32x4 w = *(const u32x4 *)(row + (int64_t)i * 16);
+    float vm = elem<BF16>(w, 0);
+#pragma unroll
+    for (int e = 1; e < EPV; ++e) vm = fmaxf(vm, elem<BF16>(w, e));
+    const float nm = fmaxf(m, vm);
+    if (nm > -INFINITY) {
+      float add = 0.f;
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) add += exp2f((elem<BF16>(w, e) - nm) * kLog2e);
+      s = (m > -INFINITY ? s * exp2f((m - nm) * kLog2e) : 0.f) + add;
+      m = nm;
+    }
+  }
+  for (int v = nvec * EPV + threadIdx.x; v < vocab; v += kThreads) {
+    const float x = load_one<BF16>(row, v);
+    const float nm = fmaxf(m, x);
+    if (nm > -INFINITY) {
+      s = (m > -INFINITY ? s * exp2f((m - nm) * kLog2e) : 0.f) + exp2f((x - nm) * kLog2e);
+      m = nm;
+    }
+  }
+  block_max_sum(m, s, sh);
+  M = m;
+  S = s;
+}
+
+// The residual's unnormalised mass at token v: max(0, p(v) - c q(v)).
+struct Residual {
+  float mp, ip, mq, iq, c;  // p = exp(x - mp) * ip, q = exp(y - mq) * iq
+  bool has_q;
+  __device__ __forceinline__ float at(float x, float y) const {
+    const float p = exp2f((x - mp) * kLog2e) * ip;
+    if (!has_q || c == 0.f) return p;
+    return fmaxf(p - c * (exp2f((y - mq) * kLog2e) * iq), 0.f);
+  }
+};
+
+// Sum over the vocabulary of the residual.
+template <bool BF16>
+__device__ float residual_mass(const char *prow, const char *qrow, int vocab, const Residual &R, Shared &sh) {
+  constexpr int EPV = BF16 ? 8 : 4;
+  const int nvec = vocab / EPV;
+  float s = 0.f;
+  for (int i = threadIdx.x; i < nvec; i += kThreads) {
+    const u32x4 w = *(const u32x4 *)(prow + (int64_t)i * 16);
+    const u32x4 z = R.has_q ? *(const u32x4 *)(qrow + (int64_t)i * 16) : w;
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) s += R.at(elem<BF16>(w, e), elem<BF16>(z, e));
+  }
+  for (int v = nvec * EPV + threadIdx.x; v < vocab; v += kThreads)
+    s += R.at(load_one<BF16>(prow, v), R.has_q ? load_one<BF16>(qrow, v) : 0.f);
+  return block_sum(s, sh);
+}
+
+// Inverse-CDF draw from the residual: the smallest v whose cumulative mass
+// (in token order) exceeds u * (total mass); the last token of nonzero mass
+// when rounding leaves the target past the end.  Thread t owns the
+// contiguous segment [t * seg, (t + 1) * seg).
+template <bool BF16>
+__device__ int residual_draw(const char *prow, const char *qrow, int vocab, const Residual &R, float u,
+                             Shared &sh) {
+  const int t = threadIdx.x;
+  const int seg = (vocab + kThreads - 1) / kThreads;
+  const int lo = min(vocab, t * seg), hi = min(vocab, lo + seg);
+  float s = 0.f;
+  int last = -1;
+  for (int v = lo; v < hi; ++v) {
+    const float r = R.at(load_one<BF16>(prow, v), R.has_q ? load_one<BF16>(qrow, v) : 0.f);
+    s += r;
+    if (r > 0.f) last = v;
+  }
+  // exclusive prefix of the segment sums (in token order) and the total
+  sh.scan[t] = s;
+  if (t == 0) sh.pick = -1;
+  __syncthreads();
+  for (int off = 1; off < kThreads; off <<= 1) {
+    const float add = t >= off ? sh.scan[t - off] : 0.f;
+    __syncthreads();
+    sh.scan[t] += add;
+    __syncthreads();
+  }
+  const float total = sh.scan[kThreads - 1];
+  const float incl = sh.scan[t];
+  const float excl = t > 0 ? sh.scan[t - 1] : 0.f;  // exactly the previous segment's end
+  const float target = u * total;
+  // the one segment whose running sum first exceeds the target
+  if (s > 0.f && excl <= target && target < incl) {
+    float acc = excl;
+    int v = lo;
+    for (; v < hi; ++v) {
+      acc += R.at(load_one<BF16>(prow, v), R.has_q ? load_one<BF16>(qrow, v) : 0.f);
+      if (acc > target) break;
+    }
+    sh.pick = min(v, last);
+  }
+  __syncthreads();
+  int pick = sh.pick;
+  if (pick < 0) {
+    // target at or past the total: the last token of nonzero mass
+    int lastv = last;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) lastv = max(lastv, __shfl_xor(lastv, off, 64));
+    if ((t & 63) == 0) sh.red_a[t >> 6] = __int_as_float(lastv);
+    __syncthreads();
+    pick = -1;
+    for (int w = 0; w < kWaves; ++w) pick = max(pick, __float_as_int(sh.red_a[w]));
+    __syncthreads();
+  }
+  return pick;
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a) {
+  __shared__ Shared sh;
+  constexpr int ESZ = BF16 ? 2 : 4;
+  const int r = blockIdx.x, t = threadIdx.x;
+  const int K = a.max_accept;
+  int32_t *alen = a.accept_len + r;
+  int32_t *otok = a.accept_tokens + (int64_t)r * K;
+  int32_t *onode = a.accept_nodes + (int64_t)r * K;
+
+  const int32_t base = a.node_indptr[r];
+  const int32_t n = a.node_indptr[r + 1] - base;
+  const bool shape_ok = n >= 1 && n <= kMaxSampledNodes && base >= 0 && base + n <= a.total_nodes;
+  if (t == 0) sh.bad = shape_ok ? 0 : 1;
+  __syncthreads();
+  if (shape_ok) {
+    for (int i = t; i < n; i += kThreads) {
+      const int32_t p = a.parent[base + i];
+      const int32_t tk = a.draft_tokens[base + i];
+      sh.parent[i] = p;
+      sh.token[i] = tk;
+      const bool ok = i == 0 ? p == -1 : (p >= 0 && p < i && tk >= 0 && tk < a.vocab);
+      if (!ok) atomicOr(&sh.bad, 1);
+    }
+  }
+  __syncthreads();
+  if (!sh.bad && t == 0) {
+    // depth of every node (parents come first), bounded by the output rows
+    int deepest = 0;
+    sh.depth[0] = 0;
+    for (int i = 1; i < n; ++i) {
+      sh.depth[i] = sh.depth[sh.parent[i]] + 1;
+      deepest = max(deepest, sh.depth[i]);
+    }
+    if (deepest > K - 1) sh.bad = 1;
+  }
+  __syncthreads();
+  if (sh.bad) {
+    for (int k = t; k < K; k += kThreads) {
+      otok[k] = -1;
+      onode[k] = -1;
+    }
+    if (t == 0) *alen = -1;
+    return;
+  }
+
+  int u = 0, len = 1;  // current node, path length
+  if (t == 0) sh.path[0] = 0;
+  while (true) {
+    const char *prow = (const char *)a.target_logits + ((int64_t)(base + u) * a.row_stride) * ESZ;
+    const char *qrow = (const char *)a.draft_logits + ((int64_t)(base + u) * a.row_stride) * ESZ;
+    int first_child = -1;
+    for (int i = u + 1; i < n; ++i)
+      if (sh.parent[i] == u) {
+        first_child = i;
+        break;
+      }
+    Residual R;
+    float sp, sq = 1.f;
+    row_stats<BF16>(prow, a.vocab, R.mp, sp, sh);
+    R.ip = 1.f / sp;
+    R.has_q = first_child >= 0;
+    R.mq = 0.f;
+    if (R.has_q) row_stats<BF16>(qrow, a.vocab, R.mq, sq, sh);
+    R.iq = 1.f / sq;
+    R.c = 0.f;
+    float S = 1.f;  // mass of the current residual (exactly 1 for p itself)
+    int next = -1;
+    for (int c = first_child; c >= 0 && c < n; ++c) {
+      if (sh.parent[c] != u) continue;
+      const int tok = sh.token[c];
+      const float pt = exp2f((load_one<BF16>(prow, tok) - R.mp) * kLog2e) * R.ip;
+      const float qt = exp2f((load_one<BF16>(qrow, tok) - R.mq) * kLog2e) * R.iq;
+      const float rt = (R.c == 0.f ? pt : fmaxf(pt - R.c * qt, 0.f)) / S;
+      if (a.u_accept[base + c] * qt < rt) {
+        next = c;
+        break;
+      }
+      Residual R2 = R;
+      R2.c = R.c + S;
+      const float S2 = residual_mass<BF16>(prow, qrow, a.vocab, R2, sh);
+      if (!(S2 > 0.f)) break;  // no mass left (rounding): draw from the residual before it
+      R = R2;
+      S = S2;
+    }
+    if (next < 0) {
+      const int v = residual_draw<BF16>(prow, qrow, a.vocab, R, a.u_bonus[base + u], sh);
+      if (t == 0) sh.out[len - 1] = v;
+      break;
+    }
+    if (t == 0) {
+      sh.out[len - 1] = sh.token[next];
+      sh.path[len] = next;
+    }
+    ++len;
+    u = next;
+  }
+  __syncthreads();
+  for (int k = t; k < K; k += kThreads) {
+    otok[k] = k < len ? sh.out[k] : -1;
+    onode[k] = k < len ? sh.path[k] : -1;
+  }
+  if (t == 0) *alen = len;
+}
+
+}  // namespace
+
+hipError_t launch_sampled_accept(const SampledArgs &a, bool bf16, hipStream_t stream) {
+  if (a.num_requests == 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL(sampled_accept_kernel<true>, dim3((unsigned)a.num_requests), dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(sampled_accept_kernel<false>, dim3((unsigned)a.num_requests), dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace adaserve

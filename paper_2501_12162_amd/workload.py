@@ -540,3 +540,24 @@ def make_beam_batch(rng: np.random.Generator, num_requests: int, beam_in: int, v
     if dead_beams:
         lp[:, beam_in - dead_beams:] = -np.inf
     return BeamBatch(logits=logits, beam_logprob=lp, vocab=vocab, dtype=dtype)
+
+
+# ---------------------------------------------------------------------------
+# Inputs of sampled-decoding verification
+# ---------------------------------------------------------------------------
+
+def make_draft_logits(rng: np.random.Generator, logits: np.ndarray, vocab: int, dtype: str,
+                      noise_std: float) -> np.ndarray:
+    """Draft-model logits shaped like ``logits``: the target's values plus
+    N(0, noise_std) noise (a draft model that mostly agrees with the target),
+    rounded to bf16 for "bf16"; columns past ``vocab`` keep the target's."""
+    x = bf16_bits_to_f32(logits) if dtype == "bf16" else np.asarray(logits, dtype=np.float32)
+    y = x.copy()
+    y[:, :vocab] += (rng.standard_normal(size=(x.shape[0], vocab), dtype=np.float32) * np.float32(noise_std))
+    return f32_to_bf16_bits(y) if dtype == "bf16" else y
+
+
+def make_uniforms(rng: np.random.Generator, n: int) -> np.ndarray:
+    """n float32 uniforms in [0, 1) (the random numbers sampled verification
+    consumes: one acceptance test per node, one bonus draw per node)."""
+    return np.minimum(rng.random(n, dtype=np.float32), np.float32(1.0) - np.float32(2.0 ** -24))

@@ -258,3 +258,37 @@ def test_beam_rejects_bad_arguments(lib, kw, code):
 def test_beam_empty_batch_is_a_noop(lib):
     assert _beam(lib, B=0, logits=None, lp=None, par=None, tok=None, out_lp=None, ws=None,
                  ws_bytes=0) == ada.ADASERVE_OK
+
+
+def _sampled(lib, **kw):
+    args = dict(B=2, T=10, indptr=FAKE, par=FAKE, draft=FAKE, tl=0x1000 * 16, dl=0x2000 * 16, stride=1024, V=1000,
+                dtype=ada.ADASERVE_BF16, ua=FAKE, ub=FAKE, K=8, alen=FAKE, tok=FAKE, nodes=FAKE)
+    args.update(kw)
+    return lib.adaserve_tree_accept_sampled(args["B"], args["T"], args["indptr"], args["par"], args["draft"],
+                                            args["tl"], args["dl"], args["stride"], args["V"], args["dtype"],
+                                            args["ua"], args["ub"], args["K"], args["alen"], args["tok"],
+                                            args["nodes"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=-1), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(T=-1), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(K=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(V=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(stride=999), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(stride=1001), ada.ADASERVE_ERR_INVALID_ARGUMENT),     # rows not 16 bytes apart
+    (dict(tl=0x1000 * 16 + 4), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(dtype=5), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(indptr=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(dl=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(ub=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(nodes=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+])
+def test_sampled_accept_rejects_bad_arguments(lib, kw, code):
+    assert _sampled(lib, **kw) == code
+    assert lib.adaserve_last_error()
+
+
+def test_sampled_accept_empty_batch_is_a_noop(lib):
+    assert _sampled(lib, B=0, T=0, indptr=None, par=None, draft=None, tl=None, dl=None, ua=None, ub=None,
+                    alen=None, tok=None, nodes=None) == ada.ADASERVE_OK

@@ -29,14 +29,14 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "sampled_hand_worked.
 
 def test_hand_worked_cases():
     for c in json.load(open(GOLDEN))["cases"]:
-        alen, tok, nodes, margin = oracle.tree_accept_sampled(
+        alen, tok, nodes, margin, cdf = oracle.tree_accept_sampled(
             node_indptr=c["node_indptr"], parent=c["parent"], draft_tokens=c["draft_tokens"],
             target_logits=np.log(np.array(c["p"])), draft_logits=np.log(np.array(c["q"])), vocab=3,
             u_accept=c["u_accept"], u_bonus=c["u_bonus"], max_accept=c["max_accept"])
         assert alen[0] == c["accept_len"], c["name"]
         assert nodes[0].tolist() == c["accept_nodes"], c["name"]
         assert tok[0].tolist() == c["accept_tokens"], c["name"]
-        assert margin[0] > 0
+        assert margin[0] > 0 and cdf[0][-1] == pytest.approx(1.0)
 
 
 def _two_level_batch(rng, trials, V, k1, k2, p_root, p_next, q_root, q_next):
@@ -73,7 +73,7 @@ def test_lossless_first_and_second_token():
     q_next = rng.dirichlet(np.ones(V), size=V)
     indptr, parent, tok, tl, dl = _two_level_batch(rng, trials, V, 3, 2, p_root, p_next, q_root, q_next)
     T = tok.size
-    alen, out, _, _ = oracle.tree_accept_sampled(
+    alen, out, _, _, _ = oracle.tree_accept_sampled(
         node_indptr=indptr, parent=parent, draft_tokens=tok, target_logits=tl, draft_logits=dl, vocab=V,
         u_accept=rng.random(T), u_bonus=rng.random(T), max_accept=4)
     assert (alen >= 1).all()
@@ -131,7 +131,7 @@ def test_draft_equal_to_target_accepts_the_first_child():
     par = random_tree(rng, 30, 5)
     logits = rng.normal(size=(30, V))
     draft = rng.integers(0, V, size=30).astype(np.int32)
-    alen, tok, nodes, _ = oracle.tree_accept_sampled(
+    alen, tok, nodes, _, _ = oracle.tree_accept_sampled(
         node_indptr=[0, 30], parent=par, draft_tokens=draft, target_logits=logits, draft_logits=logits,
         vocab=V, u_accept=rng.random(30) * 0.999, u_bonus=rng.random(30), max_accept=8)
     u, chain = 0, [0]
