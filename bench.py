@@ -370,12 +370,14 @@ def main():
     s_len = torch.empty_like(dev.accept_len)
     s_tok = torch.empty_like(dev.accept_tokens)
     s_nodes = torch.empty_like(dev.accept_nodes)
+    s_ws = torch.empty(ada.adaserve_tree_accept_sampled_workspace_bytes(b.total_nodes), dtype=torch.uint8,
+                       device="cuda")
 
     def sampled():
         ada.adaserve_tree_accept_sampled(node_indptr=dev.node_indptr, parent=dev.parent, draft_tokens=dev.draft_tokens,
                                          target_logits=rp["logits"], draft_logits=d_logits, vocab=b.vocab,
                                          u_accept=u_acc, u_bonus=u_bon, max_accept=dev.max_accept, accept_len=s_len,
-                                         accept_tokens=s_tok, accept_nodes=s_nodes)
+                                         accept_tokens=s_tok, accept_nodes=s_nodes, workspace=s_ws)
     sampled()
     torch.cuda.synchronize()
     calib_dst.copy_(calib_src)

@@ -302,7 +302,8 @@ int32_t adaserve_beam_step(int32_t num_requests, int32_t beam_in, const void *lo
  * Row u of target_logits / draft_logits ([total_nodes, row_stride], dtype)
  * holds the target / draft model's logits after node u's root path, already
  * divided by the sampling temperature; p_u / q_u are their softmax over
- * columns 0 .. vocab - 1.  Draft rows of leaves are never read.  From the
+ * columns 0 .. vocab - 1.  Draft rows of leaves are read (by the statistics
+ * pass) but never affect the result.  From the
  * root, the children of the current node u are tried in index order: child
  * c with token t = draft_tokens[c] is accepted when
  *   u_accept[c] * q_u(t) < p_res(t)
@@ -321,16 +322,23 @@ int32_t adaserve_beam_step(int32_t num_requests, int32_t beam_in, const void *lo
  * of -1 for a malformed tree (as adaserve_tree_accept), a draft token of a
  * non-root node outside [0, vocab), or a tree deeper than max_accept - 1.
  * u_accept, u_bonus: [total_nodes] fp32 (device).  Logits 16-byte aligned,
- * row_stride * element size a multiple of 16 bytes.  One workgroup walks one
- * request; requests run in parallel.
+ * row_stride * element size a multiple of 16 bytes.  workspace: at least
+ * adaserve_tree_accept_sampled_workspace_bytes(total_nodes) bytes of device
+ * memory (16 per node: every node's softmax statistics), 16-byte aligned,
+ * no initialisation needed; calls sharing a workspace must not overlap in
+ * time.  Two kernels are enqueued on `stream`: the statistics of every node
+ * (the whole chip), then the walks, one workgroup per request.
  */
+size_t adaserve_tree_accept_sampled_workspace_bytes(int32_t total_nodes);
+
 int32_t adaserve_tree_accept_sampled(int32_t num_requests, int32_t total_nodes,
                                      const int32_t *node_indptr, const int32_t *parent,
                                      const int32_t *draft_tokens, const void *target_logits,
                                      const void *draft_logits, int64_t row_stride, int32_t vocab,
                                      int32_t dtype, const float *u_accept, const float *u_bonus,
                                      int32_t max_accept, int32_t *accept_len,
-                                     int32_t *accept_tokens, int32_t *accept_nodes, void *stream);
+                                     int32_t *accept_tokens, int32_t *accept_nodes,
+                                     void *workspace, size_t workspace_bytes, void *stream);
 
 /* Message describing the last non-OK status returned on this thread. */
 const char *adaserve_last_error(void);

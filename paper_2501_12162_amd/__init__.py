@@ -41,8 +41,9 @@ SIGNATURES = {
     "adaserve_select_trees": (_I32, [_I32, _I32, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P]),
     "adaserve_beam_step_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, _I32]),
     "adaserve_beam_step": (_I32, [_I32, _I32, _P, _I64, _I32, _I32, _P, _I32, _P, _P, _P, _P, _SZ, _P]),
+    "adaserve_tree_accept_sampled_workspace_bytes": (_SZ, [_I32]),
     "adaserve_tree_accept_sampled": (_I32, [_I32, _I32, _P, _P, _P, _P, _P, _I64, _I32, _I32, _P, _P, _I32,
-                                            _P, _P, _P, _P]),
+                                            _P, _P, _P, _P, _SZ, _P]),
     "adaserve_last_error": (ctypes.c_char_p, []),
 }
 
@@ -216,11 +217,19 @@ def adaserve_beam_step(*, logits, vocab: int, beam_logprob, out_parent, out_toke
     _check(st)
 
 
+def adaserve_tree_accept_sampled_workspace_bytes(total_nodes: int) -> int:
+    n = load_library().adaserve_tree_accept_sampled_workspace_bytes(int(total_nodes))
+    if n == ctypes.c_size_t(-1).value:
+        _check(ADASERVE_ERR_INVALID_ARGUMENT)
+    return int(n)
+
+
 def adaserve_tree_accept_sampled(*, node_indptr, parent, draft_tokens, target_logits, draft_logits, vocab: int,
                                  u_accept, u_bonus, max_accept: int, accept_len, accept_tokens, accept_nodes,
-                                 stream=None) -> None:
+                                 workspace, stream=None) -> None:
     """Sampled-decoding tree verification; logits [T, row_stride] (temperature applied),
-    u_accept / u_bonus [T] float32; outputs as adaserve_tree_accept."""
+    u_accept / u_bonus [T] float32; workspace of adaserve_tree_accept_sampled_workspace_bytes(T)
+    bytes; outputs as adaserve_tree_accept."""
     B = node_indptr.shape[0] - 1
     T, stride = target_logits.shape
     if draft_logits.shape != target_logits.shape or draft_logits.dtype != target_logits.dtype:
@@ -229,5 +238,6 @@ def adaserve_tree_accept_sampled(*, node_indptr, parent, draft_tokens, target_lo
         int(B), int(parent.shape[0]), _dptr(node_indptr), _dptr(parent), _dptr(draft_tokens),
         _dptr(target_logits), _dptr(draft_logits), int(stride), int(vocab), _dtype_code(target_logits),
         _dptr(u_accept), _dptr(u_bonus), int(max_accept), _dptr(accept_len), _dptr(accept_tokens),
-        _dptr(accept_nodes), _stream(stream))
+        _dptr(accept_nodes), _dptr(workspace), int(0 if workspace is None else workspace.numel() * workspace.element_size()),
+        _stream(stream))
     _check(st)

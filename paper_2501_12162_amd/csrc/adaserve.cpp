@@ -617,12 +617,20 @@ int32_t adaserve_beam_step(int32_t num_requests, int32_t beam_in, const void *lo
   return launch_status(launch_beam_step(a, dtype == ADASERVE_BF16, (hipStream_t)stream), "beam step launch");
 }
 
+size_t adaserve_tree_accept_sampled_workspace_bytes(int32_t total_nodes) {
+  if (total_nodes < 0) {
+    fail(ADASERVE_ERR_INVALID_ARGUMENT, "total_nodes %d < 0", total_nodes);
+    return SIZE_MAX;
+  }
+  return (size_t)total_nodes * 16;
+}
+
 int32_t adaserve_tree_accept_sampled(int32_t num_requests, int32_t total_nodes, const int32_t *node_indptr,
                                      const int32_t *parent, const int32_t *draft_tokens, const void *target_logits,
                                      const void *draft_logits, int64_t row_stride, int32_t vocab, int32_t dtype,
                                      const float *u_accept, const float *u_bonus, int32_t max_accept,
                                      int32_t *accept_len, int32_t *accept_tokens, int32_t *accept_nodes,
-                                     void *stream) {
+                                     void *workspace, size_t workspace_bytes, void *stream) {
   if (num_requests < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_requests %d < 0", num_requests);
   if (total_nodes < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "total_nodes %d < 0", total_nodes);
   if (max_accept < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "max_accept %d < 1", max_accept);
@@ -642,6 +650,11 @@ int32_t adaserve_tree_accept_sampled(int32_t num_requests, int32_t total_nodes, 
   if (!aligned(target_logits, 16) || !aligned(draft_logits, 16) || (row_stride * esz) % 16 != 0)
     return fail(ADASERVE_ERR_INVALID_ARGUMENT,
                 "logits must be 16-byte aligned with rows a multiple of 16 bytes apart");
+  const size_t need = (size_t)total_nodes * 16;
+  if (need > 0 && (!workspace || workspace_bytes < need))
+    return fail(ADASERVE_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace ? workspace_bytes : (size_t)0,
+                need);
+  if (need > 0 && !aligned(workspace, 16)) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "workspace must be 16-byte aligned");
   const int32_t st = check_device();
   if (st != ADASERVE_OK) return st;
   SampledArgs a;
@@ -660,6 +673,7 @@ int32_t adaserve_tree_accept_sampled(int32_t num_requests, int32_t total_nodes, 
   a.accept_len = accept_len;
   a.accept_tokens = accept_tokens;
   a.accept_nodes = accept_nodes;
+  a.stats = (float4 *)workspace;
   return launch_status(launch_sampled_accept(a, dtype == ADASERVE_BF16, (hipStream_t)stream), "sampled accept launch");
 }
 

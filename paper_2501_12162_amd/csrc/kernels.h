@@ -149,6 +149,7 @@ struct SampledArgs {
   int32_t *accept_len;          // [B]
   int32_t *accept_tokens;       // [B, max_accept]
   int32_t *accept_nodes;        // [B, max_accept]
+  float4 *stats;                // [total_nodes] workspace: (max_p, sum_p, max_q, sum_q)
 };
 
 hipError_t launch_sampled_accept(const SampledArgs &a, bool bf16, hipStream_t stream);

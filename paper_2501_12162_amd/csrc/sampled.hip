@@ -13,11 +13,13 @@
 // Every residual has the closed form max(0, p - c q) / S: after a
 // rejection c grows by the previous S and S is the new residual's mass
 // (if p_res = r/S with r = max(0, p - c q), then max(0, p_res - q) is
-// proportional to max(0, p - (c + S) q)).  So a node costs one pass over its
-// two logits rows for the softmax statistics, one more pass per rejection
-// (the new S), and the bonus draw two passes (segment sums, then a scan of
-// the one segment that holds the target).  One workgroup of 1024 threads
-// walks one request; the walk is sequential, requests run side by side.
+// proportional to max(0, p - (c + S) q)).  A first kernel computes every
+// node's softmax statistics (max and exp-sum of its target and draft rows)
+// across the whole chip; the walk -- one workgroup of 1024 threads per
+// request -- then reads them, so an acceptance test costs two logits, a
+// rejection one pass over the node's two rows (the new S), and the bonus
+// draw two passes (segment sums, then a scan of the one segment that holds
+// the target).
 #include <limits.h>
 
 #include "device_common.h"
@@ -28,6 +30,7 @@ namespace adaserve {
 namespace {
 
 constexpr int kThreads = 1024;
+constexpr int kStatsThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -69,72 +72,16 @@ __device__ float block_sum(float v, Shared &sh) {
   return t;
 }
 
-// Block-wide (max, sum of exp(x - max)) merge of per-thread pairs.
-__device__ void block_max_sum(float &m, float &s, Shared &sh) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  float wm = m;
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) wm = fmaxf(wm, __shfl_xor(wm, off, 64));
-  float ws = wm > -INFINITY && m > -INFINITY ? s * exp2f((m - wm) * kLog2e) : 0.f;
-  ws = wave_sum(ws);
-  if (lane == 0) {
-    sh.red_a[wave] = wm;
-    sh.red_b[wave] = ws;
-  }
-  __syncthreads();
-  float M = -INFINITY;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sh.red_a[w]);
-  float S = 0.f;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w)
-    if (sh.red_a[w] > -INFINITY) S += sh.red_b[w] * exp2f((sh.red_a[w] - M) * kLog2e);
-  __syncthreads();
-  m = M;
-  s = S;
-}
-
-// Softmax statistics (max, sum of exp(x - max)) of one logits row.
-template <bool BF16>
-__device__ void row_stats(const char *row, int vocab, float &M, float &S, Shared &sh) {
-  constexpr int EPV = BF16 ? 8 : 4;
-  const int nvec = vocab / EPV;
-  float m = -INFINITY, s = 0.f;
-  for (int i = threadIdx.x; i < nvec; i += kThreads) {
-    const u32x4 w = *(const u32x4 *)(row + (int64_t)i * 16);
-    float vm = elem<BF16>(w, 0);
-#pragma unroll
-    for (int e = 1; e < EPV; ++e) vm = fmaxf(vm, elem<BF16>(w, e));
-    const float nm = fmaxf(m, vm);
-    if (nm > -INFINITY) {
-      float add = 0.f;
-#pragma unroll
-      for (int e = 0; e < EPV; ++e) add += exp2f((elem<BF16>(w, e) - nm) * kLog2e);
-      s = (m > -INFINITY ? s * exp2f((m - nm) * kLog2e) : 0.f) + add;
-      m = nm;
-    }
-  }
-  for (int v = nvec * EPV + threadIdx.x; v < vocab; v += kThreads) {
-    const float x = load_one<BF16>(row, v);
-    const float nm = fmaxf(m, x);
-    if (nm > -INFINITY) {
-      s = (m > -INFINITY ? s * exp2f((m - nm) * kLog2e) : 0.f) + exp2f((x - nm) * kLog2e);
-      m = nm;
-    }
-  }
-  block_max_sum(m, s, sh);
-  M = m;
-  S = s;
-}
-
 // The residual's unnormalised mass at token v: max(0, p(v) - c q(v)).
+// (Bulk sums use the hardware exp2, which flushes results below 2^-126 to
+// zero: such terms are far below the sums' rounding.)
 struct Residual {
   float mp, ip, mq, iq, c;  // p = exp(x - mp) * ip, q = exp(y - mq) * iq
   bool has_q;
   __device__ __forceinline__ float at(float x, float y) const {
-    const float p = exp2f((x - mp) * kLog2e) * ip;
+    const float p = __builtin_amdgcn_exp2f((x - mp) * kLog2e) * ip;
     if (!has_q || c == 0.f) return p;
-    return fmaxf(p - c * (exp2f((y - mq) * kLog2e) * iq), 0.f);
+    return fmaxf(p - c * (__builtin_amdgcn_exp2f((y - mq) * kLog2e) * iq), 0.f);
   }
 };
 
@@ -144,7 +91,21 @@ __device__ float residual_mass(const char *prow, const char *qrow, int vocab, co
   constexpr int EPV = BF16 ? 8 : 4;
   const int nvec = vocab / EPV;
   float s = 0.f;
-  for (int i = threadIdx.x; i < nvec; i += kThreads) {
+  int i = threadIdx.x;
+  // four vectors of each row in flight per thread
+  for (; i + 3 * kThreads < nvec; i += 4 * kThreads) {
+    u32x4 w[4], z[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      w[k] = *(const u32x4 *)(prow + (int64_t)(i + k * kThreads) * 16);
+      z[k] = R.has_q ? *(const u32x4 *)(qrow + (int64_t)(i + k * kThreads) * 16) : w[k];
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) s += R.at(elem<BF16>(w[k], e), elem<BF16>(z[k], e));
+  }
+  for (; i < nvec; i += kThreads) {
     const u32x4 w = *(const u32x4 *)(prow + (int64_t)i * 16);
     const u32x4 z = R.has_q ? *(const u32x4 *)(qrow + (int64_t)i * 16) : w;
 #pragma unroll
@@ -158,21 +119,60 @@ __device__ float residual_mass(const char *prow, const char *qrow, int vocab, co
 // Inverse-CDF draw from the residual: the smallest v whose cumulative mass
 // (in token order) exceeds u * (total mass); the last token of nonzero mass
 // when rounding leaves the target past the end.  Thread t owns the
-// contiguous segment [t * seg, (t + 1) * seg).
+// contiguous segment [t * seg, (t + 1) * seg), seg a multiple of the
+// 16-byte vector, read with vector loads.
 template <bool BF16>
 __device__ int residual_draw(const char *prow, const char *qrow, int vocab, const Residual &R, float u,
                              Shared &sh) {
+  constexpr int EPV = BF16 ? 8 : 4;
   const int t = threadIdx.x;
-  const int seg = (vocab + kThreads - 1) / kThreads;
+  const int seg = ((vocab + kThreads - 1) / kThreads + EPV - 1) / EPV * EPV;
   const int lo = min(vocab, t * seg), hi = min(vocab, lo + seg);
-  float s = 0.f;
-  int last = -1;
-  for (int v = lo; v < hi; ++v) {
-    const float r = R.at(load_one<BF16>(prow, v), R.has_q ? load_one<BF16>(qrow, v) : 0.f);
-    s += r;
-    if (r > 0.f) last = v;
-  }
-  // exclusive prefix of the segment sums (in token order) and the total
+  auto seg_pass = [&](float start, float target, bool find, int &found, int &last) {
+    float acc = start;
+    found = -1;
+    last = -1;
+    int v = lo;
+    // four vectors of each row in flight per thread
+    for (; v + 4 * EPV <= hi; v += 4 * EPV) {
+      u32x4 w[4], z[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        w[k] = *(const u32x4 *)(prow + (int64_t)(v + k * EPV) * (BF16 ? 2 : 4));
+        z[k] = R.has_q ? *(const u32x4 *)(qrow + (int64_t)(v + k * EPV) * (BF16 ? 2 : 4)) : w[k];
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) {
+          const float r = R.at(elem<BF16>(w[k], e), elem<BF16>(z[k], e));
+          acc += r;
+          if (r > 0.f) last = v + k * EPV + e;
+          if (find && found < 0 && acc > target) found = v + k * EPV + e;
+        }
+    }
+    for (; v + EPV <= hi; v += EPV) {
+      const u32x4 w = *(const u32x4 *)(prow + (int64_t)v * (BF16 ? 2 : 4));
+      const u32x4 z = R.has_q ? *(const u32x4 *)(qrow + (int64_t)v * (BF16 ? 2 : 4)) : w;
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) {
+        const float r = R.at(elem<BF16>(w, e), elem<BF16>(z, e));
+        acc += r;
+        if (r > 0.f) last = v + e;
+        if (find && found < 0 && acc > target) found = v + e;
+      }
+    }
+    for (; v < hi; ++v) {
+      const float r = R.at(load_one<BF16>(prow, v), R.has_q ? load_one<BF16>(qrow, v) : 0.f);
+      acc += r;
+      if (r > 0.f) last = v;
+      if (find && found < 0 && acc > target) found = v;
+    }
+    return acc;
+  };
+  int found, last;
+  const float s = seg_pass(0.f, 0.f, false, found, last);
+  // inclusive prefix of the segment sums (in token order) and the total
   sh.scan[t] = s;
   if (t == 0) sh.pick = -1;
   __syncthreads();
@@ -188,13 +188,9 @@ __device__ int residual_draw(const char *prow, const char *qrow, int vocab, cons
   const float target = u * total;
   // the one segment whose running sum first exceeds the target
   if (s > 0.f && excl <= target && target < incl) {
-    float acc = excl;
-    int v = lo;
-    for (; v < hi; ++v) {
-      acc += R.at(load_one<BF16>(prow, v), R.has_q ? load_one<BF16>(qrow, v) : 0.f);
-      if (acc > target) break;
-    }
-    sh.pick = min(v, last);
+    int f, l2;
+    seg_pass(excl, target, true, f, l2);
+    sh.pick = f >= 0 ? min(f, last) : last;
   }
   __syncthreads();
   int pick = sh.pick;
@@ -210,6 +206,88 @@ __device__ int residual_draw(const char *prow, const char *qrow, int vocab, cons
     __syncthreads();
   }
   return pick;
+}
+
+// Softmax statistics of every node's target and draft rows: one workgroup
+// per node, both rows in one pass.  stats[node] = (max_p, sum_p, max_q, sum_q).
+template <bool BF16>
+__global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArgs a) {
+  constexpr int EPV = BF16 ? 8 : 4;
+  constexpr int ESZ = BF16 ? 2 : 4;
+  __shared__ float red[4][kStatsThreads / 64];
+  const int node = blockIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const char *prow = (const char *)a.target_logits + (int64_t)node * a.row_stride * ESZ;
+  const char *qrow = (const char *)a.draft_logits + (int64_t)node * a.row_stride * ESZ;
+  float mp = -INFINITY, sp = 0.f, mq = -INFINITY, sq = 0.f;
+  auto add = [](float &m, float &s, float x) {
+    const float nm = fmaxf(m, x);
+    if (nm > -INFINITY) {
+      s = (m > -INFINITY ? s * exp2f((m - nm) * kLog2e) : 0.f) + exp2f((x - nm) * kLog2e);
+      m = nm;
+    }
+  };
+  const int nvec = a.vocab / EPV;
+#pragma unroll 4
+  for (int i = t; i < nvec; i += kStatsThreads) {
+    const u32x4 w = *(const u32x4 *)(prow + (int64_t)i * 16);
+    const u32x4 z = *(const u32x4 *)(qrow + (int64_t)i * 16);
+    float wm = elem<BF16>(w, 0), zm = elem<BF16>(z, 0);
+#pragma unroll
+    for (int e = 1; e < EPV; ++e) {
+      wm = fmaxf(wm, elem<BF16>(w, e));
+      zm = fmaxf(zm, elem<BF16>(z, e));
+    }
+    const float nmp = fmaxf(mp, wm), nmq = fmaxf(mq, zm);
+    if (nmp > -INFINITY) {
+      float acc = 0.f;
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) acc += __builtin_amdgcn_exp2f((elem<BF16>(w, e) - nmp) * kLog2e);
+      sp = (mp > -INFINITY ? sp * __builtin_amdgcn_exp2f((mp - nmp) * kLog2e) : 0.f) + acc;
+      mp = nmp;
+    }
+    if (nmq > -INFINITY) {
+      float acc = 0.f;
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) acc += __builtin_amdgcn_exp2f((elem<BF16>(z, e) - nmq) * kLog2e);
+      sq = (mq > -INFINITY ? sq * __builtin_amdgcn_exp2f((mq - nmq) * kLog2e) : 0.f) + acc;
+      mq = nmq;
+    }
+  }
+  for (int v = nvec * EPV + t; v < a.vocab; v += kStatsThreads) {
+    add(mp, sp, load_one<BF16>(prow, v));
+    add(mq, sq, load_one<BF16>(qrow, v));
+  }
+  // (max, sum) pairs over the workgroup
+  float wmp = mp, wmq = mq;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    wmp = fmaxf(wmp, __shfl_xor(wmp, o, 64));
+    wmq = fmaxf(wmq, __shfl_xor(wmq, o, 64));
+  }
+  float wsp = wmp > -INFINITY && mp > -INFINITY ? sp * exp2f((mp - wmp) * kLog2e) : 0.f;
+  float wsq = wmq > -INFINITY && mq > -INFINITY ? sq * exp2f((mq - wmq) * kLog2e) : 0.f;
+  wsp = wave_sum(wsp);
+  wsq = wave_sum(wsq);
+  if (lane == 0) {
+    red[0][wave] = wmp;
+    red[1][wave] = wsp;
+    red[2][wave] = wmq;
+    red[3][wave] = wsq;
+  }
+  __syncthreads();
+  if (t == 0) {
+    float Mp = -INFINITY, Mq = -INFINITY, Sp = 0.f, Sq = 0.f;
+    for (int w = 0; w < kStatsThreads / 64; ++w) {
+      Mp = fmaxf(Mp, red[0][w]);
+      Mq = fmaxf(Mq, red[2][w]);
+    }
+    for (int w = 0; w < kStatsThreads / 64; ++w) {
+      if (red[0][w] > -INFINITY) Sp += red[1][w] * exp2f((red[0][w] - Mp) * kLog2e);
+      if (red[2][w] > -INFINITY) Sq += red[3][w] * exp2f((red[2][w] - Mq) * kLog2e);
+    }
+    a.stats[node] = make_float4(Mp, Sp, Mq, Sq);
+  }
 }
 
 template <bool BF16>
@@ -269,14 +347,13 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
         first_child = i;
         break;
       }
+    const float4 st = a.stats[base + u];
     Residual R;
-    float sp, sq = 1.f;
-    row_stats<BF16>(prow, a.vocab, R.mp, sp, sh);
-    R.ip = 1.f / sp;
+    R.mp = st.x;
+    R.ip = 1.f / st.y;
     R.has_q = first_child >= 0;
-    R.mq = 0.f;
-    if (R.has_q) row_stats<BF16>(qrow, a.vocab, R.mq, sq, sh);
-    R.iq = 1.f / sq;
+    R.mq = st.z;
+    R.iq = 1.f / st.w;
     R.c = 0.f;
     float S = 1.f;  // mass of the current residual (exactly 1 for p itself)
     int next = -1;
@@ -321,6 +398,14 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
 
 hipError_t launch_sampled_accept(const SampledArgs &a, bool bf16, hipStream_t stream) {
   if (a.num_requests == 0) return hipSuccess;
+  if (a.total_nodes > 0) {
+    if (bf16)
+      hipLaunchKernelGGL(sampled_stats_kernel<true>, dim3((unsigned)a.total_nodes), dim3(kStatsThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL(sampled_stats_kernel<false>, dim3((unsigned)a.total_nodes), dim3(kStatsThreads), 0, stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   if (bf16)
     hipLaunchKernelGGL(sampled_accept_kernel<true>, dim3((unsigned)a.num_requests), dim3(kThreads), 0, stream, a);
   else

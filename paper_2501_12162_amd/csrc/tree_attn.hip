@@ -737,74 +737,152 @@ __global__ __launch_bounds__(kThreads) void tree_attn_combine_kernel(TreeAttnArg
   }
 }
 
-// fp32 path: one wave per (node, q-head), exact fp32 arithmetic on the
+// fp32 path: one workgroup per (node, q-head), exact fp32 arithmetic on the
 // vector ALUs (small shapes; the matrix cores have no fp32 input path that
-// keeps full precision for Q.K).
+// keeps full precision for Q.K).  The node's keys -- its prefix, then its
+// root path -- are taken in chunks of 1024: every thread scores whole keys
+// (a dot product over the head dim), the chunk's softmax weights go to LDS,
+// then thread (group g, column d) accumulates column d of the weighted
+// values over every G-th key; an online softmax joins the chunks.
 template <int D>
-__global__ __launch_bounds__(64) void tree_attn_f32_kernel(TreeAttnArgs a) {
-  constexpr int PER = D / 64;
+__global__ __launch_bounds__(256) void tree_attn_f32_kernel(TreeAttnArgs a) {
+  constexpr int kT = 256;
+  constexpr int G = kT / D;       // key groups of the value accumulation
+  constexpr int CH = 1024;        // keys per chunk
+  __shared__ float qs[D];
+  __shared__ float ps[CH];
+  __shared__ int64_t rowoff[CH];  // >= 0: element offset in the page pool; -1: zero key; <= -2: tree row
+  __shared__ int32_t path[kMaxTreeNodes];
+  __shared__ float red[kT / 64];
+  __shared__ float part[kT];
+  __shared__ int32_t info[4];     // request, node base, path length, ok
   const int64_t idx = blockIdx.x;
   const int32_t node = (int32_t)(idx / a.num_q_heads);
   const int32_t h = (int32_t)(idx % a.num_q_heads);
   if (node >= a.total_nodes) return;
-  const int lane = threadIdx.x;
-  // request owning this node
-  int lo = 0, hi = a.num_requests - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (a.node_indptr[mid] <= node) lo = mid; else hi = mid - 1;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  if (t == 0) {
+    // request owning this node, then the node's root path
+    int lo = 0, hi = a.num_requests - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (a.node_indptr[mid] <= node) lo = mid; else hi = mid - 1;
+    }
+    const int32_t base = a.node_indptr[lo];
+    const int32_t n = a.node_indptr[lo + 1] - base;
+    int ok = node >= base && node < base + n && n <= kMaxTreeNodes;
+    int len = 0;
+    if (ok) {
+      int v = node - base;
+      for (int step = 0; step < kMaxTreeNodes; ++step) {
+        path[len++] = v;
+        if (v == 0) break;
+        const int p = a.parent[base + v];
+        if (p < 0 || p >= v) break;
+        v = p;
+      }
+    }
+    info[0] = lo;
+    info[1] = base;
+    info[2] = len;
+    info[3] = ok;
   }
-  const int r = lo;
-  const int32_t base = a.node_indptr[r];
-  const int32_t n = a.node_indptr[r + 1] - base;
-  if (node < base || node >= base + n || n > kMaxTreeNodes) return;
-  const int32_t L = max(a.prefix_len[r], 0);
   const int g = h / a.group;
   const float *q = (const float *)a.q + ((int64_t)node * a.num_q_heads + h) * D;
-  float qv[PER], acc[PER];
+  for (int d = t; d < D; d += kT) qs[d] = q[d];
+  __syncthreads();
+  if (!info[3]) return;
+  const int r = info[0], base = info[1], npath = info[2];
+  const int32_t L = max(a.prefix_len[r], 0);
+  const int32_t nkeys = L + npath;
+  const float *kp = (const float *)a.k_pages, *vp = (const float *)a.v_pages;
+  const float *kt = (const float *)a.k_tree, *vt = (const float *)a.v_tree;
+  const int col = t % D, grp = t / D;
+  float m = -INFINITY, l = 0.f, acc = 0.f;
+  for (int32_t k0 = 0; k0 < nkeys; k0 += CH) {
+    const int n = min(CH, nkeys - k0);
+    float cmax = -INFINITY;
+    for (int j = t; j < n; j += kT) {
+      const int32_t key = k0 + j;
+      int64_t off;
+      const float *kr;
+      if (key < L) {
+        const int32_t e = key / kPageSize;
+        const int32_t pg = e < a.bt_stride ? a.block_table[(int64_t)r * a.bt_stride + e] : -1;
+        off = (pg < 0 || pg >= a.num_pages) ? -1
+              : (((int64_t)pg * a.num_kv_heads + g) * kPageSize + key % kPageSize) * D;
+        kr = off >= 0 ? kp + off : nullptr;
+      } else {
+        const int64_t toff = ((int64_t)(base + path[key - L]) * a.num_kv_heads + g) * D;
+        off = -2 - toff;
+        kr = kt + toff;
+      }
+      float sc = 0.f;
+      if (kr) {
 #pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    qv[i] = q[lane + 64 * i];
-    acc[i] = 0.f;
-  }
-  float m = -INFINITY, l = 0.f;
-  auto visit = [&](const float *kp, const float *vp) {
-    float s = 0.f;
-    if (kp) {
-#pragma unroll
-      for (int i = 0; i < PER; ++i) s += qv[i] * kp[lane + 64 * i];
+        for (int d = 0; d < D; d += 4) {
+          const f32x4 kv = *(const f32x4 *)(kr + d);
+          sc = fmaf(qs[d], kv[0], sc);
+          sc = fmaf(qs[d + 1], kv[1], sc);
+          sc = fmaf(qs[d + 2], kv[2], sc);
+          sc = fmaf(qs[d + 3], kv[3], sc);
+        }
+      }
+      sc *= a.sm_scale;
+      ps[j] = sc;
+      rowoff[j] = off;
+      cmax = fmaxf(cmax, sc);
     }
-    s = wave_sum(s) * a.sm_scale;
-    const float m_new = fmaxf(m, s);
-    const float alpha = expf(m - m_new);
-    const float p = expf(s - m_new);
-    l = l * alpha + p;
 #pragma unroll
-    for (int i = 0; i < PER; ++i) acc[i] = acc[i] * alpha + (vp ? p * vp[lane + 64 * i] : 0.f);
-    m = m_new;
-  };
-  for (int32_t t = 0; t < L; ++t) {
-    int32_t p = t / kPageSize < a.bt_stride ? a.block_table[(int64_t)r * a.bt_stride + t / kPageSize] : -1;
-    if (p < 0 || p >= a.num_pages) {
-      visit(nullptr, nullptr);
-    } else {
-      const int64_t off = (((int64_t)p * a.num_kv_heads + g) * kPageSize + t % kPageSize) * D;
-      visit((const float *)a.k_pages + off, (const float *)a.v_pages + off);
+    for (int o = 32; o >= 1; o >>= 1) cmax = fmaxf(cmax, __shfl_xor(cmax, o, 64));
+    if (lane == 0) red[wave] = cmax;
+    __syncthreads();
+    float mn = m;
+#pragma unroll
+    for (int w = 0; w < kT / 64; ++w) mn = fmaxf(mn, red[w]);
+    __syncthreads();
+    const float alpha = m > -INFINITY ? expf(m - mn) : 0.f;
+    float lsum = 0.f;
+    for (int j = t; j < n; j += kT) {
+      const float p = expf(ps[j] - mn);
+      ps[j] = p;
+      lsum += p;
     }
-  }
-  int v = node - base;
-  for (int step = 0; step < kMaxTreeNodes; ++step) {
-    const int64_t off = ((int64_t)(base + v) * a.num_kv_heads + g) * D;
-    visit((const float *)a.k_tree + off, (const float *)a.v_tree + off);
-    if (v == 0) break;
-    const int p = a.parent[base + v];
-    if (p < 0 || p >= v) break;
-    v = p;
-  }
-  float *o = (float *)a.out + ((int64_t)node * a.num_q_heads + h) * D;
-  const float inv = l > 0.f ? 1.f / l : 0.f;
+    lsum = wave_sum(lsum);
+    if (lane == 0) red[wave] = lsum;
+    __syncthreads();
+    float csum = 0.f;
 #pragma unroll
-  for (int i = 0; i < PER; ++i) o[lane + 64 * i] = acc[i] * inv;
+    for (int w = 0; w < kT / 64; ++w) csum += red[w];
+    l = l * alpha + csum;
+    acc *= alpha;
+    m = mn;
+    if (grp < G)
+      for (int j0 = grp; j0 < n; j0 += 8 * G) {
+        // eight keys' loads in flight before their products
+        float pv[8], vv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int j = j0 + u * G;
+          const int64_t off = j < n ? rowoff[j] : -1;
+          const float *src = off >= 0 ? vp + off + col : off == -1 ? vt + col : vt + (-2 - off) + col;
+          pv[u] = j < n && off != -1 ? ps[j] : 0.f;
+          vv[u] = *src;  // a zero row reads tree row 0 and weighs it 0 below
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc = pv[u] != 0.f ? fmaf(pv[u], vv[u], acc) : acc;
+      }
+    __syncthreads();  // ps, rowoff and red are rewritten by the next chunk
+  }
+  part[t] = acc;
+  __syncthreads();
+  if (t < D) {
+    float o = 0.f;
+#pragma unroll
+    for (int k = 0; k < G; ++k) o += part[k * D + t];
+    float *out = (float *)a.out + ((int64_t)node * a.num_q_heads + h) * D;
+    out[t] = l > 0.f ? o / l : 0.f;
+  }
 }
 
 }  // namespace
@@ -850,7 +928,7 @@ hipError_t launch_tree_attn_bf16(TreeAttnArgs &a, int head_dim, bool needs_combi
 hipError_t launch_tree_attn_f32(const TreeAttnArgs &a, int head_dim, hipStream_t stream) {
   const int64_t blocks = (int64_t)a.total_nodes * a.num_q_heads;
   if (blocks == 0) return hipSuccess;
-  const dim3 grid((unsigned)blocks), block(64);
+  const dim3 grid((unsigned)blocks), block(256);
   if (head_dim == 128)
     hipLaunchKernelGGL(tree_attn_f32_kernel<128>, grid, block, 0, stream, a);
   else

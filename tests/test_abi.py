@@ -262,12 +262,13 @@ def test_beam_empty_batch_is_a_noop(lib):
 
 def _sampled(lib, **kw):
     args = dict(B=2, T=10, indptr=FAKE, par=FAKE, draft=FAKE, tl=0x1000 * 16, dl=0x2000 * 16, stride=1024, V=1000,
-                dtype=ada.ADASERVE_BF16, ua=FAKE, ub=FAKE, K=8, alen=FAKE, tok=FAKE, nodes=FAKE)
+                dtype=ada.ADASERVE_BF16, ua=FAKE, ub=FAKE, K=8, alen=FAKE, tok=FAKE, nodes=FAKE, ws=0x100000,
+                ws_bytes=160)
     args.update(kw)
     return lib.adaserve_tree_accept_sampled(args["B"], args["T"], args["indptr"], args["par"], args["draft"],
                                             args["tl"], args["dl"], args["stride"], args["V"], args["dtype"],
                                             args["ua"], args["ub"], args["K"], args["alen"], args["tok"],
-                                            args["nodes"], None)
+                                            args["nodes"], args["ws"], args["ws_bytes"], None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -283,6 +284,9 @@ def _sampled(lib, **kw):
     (dict(dl=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
     (dict(ub=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
     (dict(nodes=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(ws=None), ada.ADASERVE_ERR_WORKSPACE),
+    (dict(ws_bytes=159), ada.ADASERVE_ERR_WORKSPACE),
+    (dict(ws=0x100000 + 8), ada.ADASERVE_ERR_INVALID_ARGUMENT),   # workspace not 16-byte aligned
 ])
 def test_sampled_accept_rejects_bad_arguments(lib, kw, code):
     assert _sampled(lib, **kw) == code
@@ -291,4 +295,10 @@ def test_sampled_accept_rejects_bad_arguments(lib, kw, code):
 
 def test_sampled_accept_empty_batch_is_a_noop(lib):
     assert _sampled(lib, B=0, T=0, indptr=None, par=None, draft=None, tl=None, dl=None, ua=None, ub=None,
-                    alen=None, tok=None, nodes=None) == ada.ADASERVE_OK
+                    alen=None, tok=None, nodes=None, ws=None, ws_bytes=0) == ada.ADASERVE_OK
+
+
+def test_sampled_accept_workspace_query(lib):
+    assert lib.adaserve_tree_accept_sampled_workspace_bytes(0) == 0
+    assert lib.adaserve_tree_accept_sampled_workspace_bytes(586) == 586 * 16
+    assert lib.adaserve_tree_accept_sampled_workspace_bytes(-1) == SIZE_MAX

@@ -52,12 +52,14 @@ def _run(torch, indptr, parent, draft, tl, dl, vocab, ua, ub, max_accept):
     alen = torch.full((B,), -7, dtype=torch.int32, device="cuda")
     tok = torch.full((B, max_accept), -7, dtype=torch.int32, device="cuda")
     nodes = torch.full((B, max_accept), -7, dtype=torch.int32, device="cuda")
+    T = len(parent)
+    ws = torch.empty(max(16, ada.adaserve_tree_accept_sampled_workspace_bytes(T)), dtype=torch.uint8, device="cuda")
     ada.adaserve_tree_accept_sampled(
         node_indptr=_dev(torch, np.asarray(indptr, np.int32)), parent=_dev(torch, np.asarray(parent, np.int32)),
         draft_tokens=_dev(torch, np.asarray(draft, np.int32)), target_logits=_dev(torch, tl),
         draft_logits=_dev(torch, dl), vocab=vocab, u_accept=_dev(torch, np.asarray(ua, np.float32)),
         u_bonus=_dev(torch, np.asarray(ub, np.float32)), max_accept=max_accept, accept_len=alen,
-        accept_tokens=tok, accept_nodes=nodes)
+        accept_tokens=tok, accept_nodes=nodes, workspace=ws)
     torch.cuda.synchronize()
     return alen.cpu().numpy(), tok.cpu().numpy(), nodes.cpu().numpy()
 
