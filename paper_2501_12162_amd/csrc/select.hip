@@ -4,11 +4,12 @@
 // verification scores.
 //
 // The whole batch is one workgroup of 1024 threads with everything in LDS
-// (at most 8192 candidates): candidates are ranked by one bitonic sort on a
-// 64-bit key (request, path probability descending, depth, index), so each
-// request's candidates sit in a contiguous best-first segment; one thread
-// per request walks its segment adding path probabilities in float32 to
-// find how many picks reach its need; one thread deals the budget to the
+// (at most 8192 candidates): each request's candidates (at most 127) are
+// ranked by one wave with a bitonic network in registers on a 64-bit key
+// (path probability descending, depth, index) and written to the request's
+// contiguous best-first segment; one thread per request walks its segment
+// adding path probabilities in float32 to find how many picks reach its
+// need; one thread deals the budget to the
 // requests in descending order of need; a second bitonic sort ranks the
 // remaining candidates of the whole batch (probability descending, depth,
 // request, index) and the first `remaining budget` of them are added.
@@ -117,25 +118,7 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
       }
       depth[i] = (uint8_t)d;
     }
-  // sort 1: (request, probability descending, depth, index)
-  int n = 2;
-  while (n < C) n <<= 1;
-  for (int i = tid; i < n; i += kThreads) {
-    uint64_t k = kNone;
-    if (good && i < C) {
-      const int r = request_of(i);
-      if (ok[r])
-        k = ((uint64_t)r << 55) | ((uint64_t)(~__float_as_uint(prob[i])) << 23) |
-            ((uint64_t)depth[i] << 16) | ((uint64_t)(i - lo[r]) << 9);
-    }
-    key[i] = k;
-  }
-  __syncthreads();
-  bitonic_sort(key, n);
-
-  // segment starts (well-formed requests in index order), then each request's
-  // SLO picks: add the best remaining candidate while the float32 sum of the
-  // added probabilities is below its need and the tree is under n_max nodes
+  // segment starts: well-formed requests in index order
   if (tid == 0) {
     int s = 0;
     for (int r = 0; r < B; ++r) {
@@ -144,6 +127,50 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
     }
   }
   __syncthreads();
+  // sort 1, per request: (probability descending, depth, index); one wave
+  // sorts a request's (at most 127) keys in registers, two per lane, with a
+  // bitonic network, and writes them to the request's segment
+  {
+    const int lane = tid & 63, wave = tid >> 6;
+    for (int r = wave; r < B; r += kThreads / 64) {
+      if (!ok[r]) continue;
+      const int nr = lo[r + 1] - lo[r];
+      uint64_t k2[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int j = lane + 64 * h;
+        const int i = lo[r] + j;
+        k2[h] = j < nr ? ((uint64_t)(~__float_as_uint(prob[i])) << 23) | ((uint64_t)depth[i] << 16) |
+                             ((uint64_t)j << 9)
+                       : kNone;
+      }
+      for (int k = 2; k <= 128; k <<= 1)
+        for (int j = k >> 1; j > 0; j >>= 1) {
+          uint64_t nk[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int e = lane + 64 * h;   // element index; its partner is e ^ j
+            const uint64_t other = j == 64 ? k2[h ^ 1] : (uint64_t)__shfl_xor((unsigned long long)k2[h], j, 64);
+            const bool lower = (e & j) == 0;
+            const bool up = (e & k) == 0;   // ascending block
+            const uint64_t mn = other < k2[h] ? other : k2[h], mx = other < k2[h] ? k2[h] : other;
+            nk[h] = (lower == up) ? mn : mx;
+          }
+          k2[0] = nk[0];
+          k2[1] = nk[1];
+        }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int j = lane + 64 * h;
+        if (j < nr) key[seg[r] + j] = k2[h];
+      }
+    }
+  }
+  __syncthreads();
+
+  // each request's SLO picks: add the best remaining candidate while the
+  // float32 sum of the added probabilities is below its need and the tree is
+  // under n_max nodes
   for (int r = tid; r < B; r += kThreads) {
     int k = 0;
     if (ok[r]) {
@@ -194,6 +221,8 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
   __syncthreads();
 
   // sort 2: the remaining candidates of the batch, best first
+  int n = 2;
+  while (n < C) n <<= 1;
   for (int i = tid; i < n; i += kThreads) {
     uint64_t k = kNone;
     if (good && i < C && !picked[i]) {
