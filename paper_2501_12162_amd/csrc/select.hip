@@ -4,15 +4,22 @@
 // verification scores.
 //
 // The whole batch is one workgroup of 1024 threads with everything in LDS
-// (at most 8192 candidates): each request's candidates (at most 127) are
-// ranked by one wave with a bitonic network in registers on a 64-bit key
-// (path probability descending, depth, index) and written to the request's
-// contiguous best-first segment; one thread per request walks its segment
-// adding path probabilities in float32 to find how many picks reach its
-// need; one thread deals the budget to the
-// requests in descending order of need; a second bitonic sort ranks the
-// remaining candidates of the whole batch (probability descending, depth,
-// request, index) and the first `remaining budget` of them are added.
+// (at most 8192 candidates):
+// * each candidate gets a 55-bit key (path probability descending, depth,
+//   index) and finds its place in its request's best-first order by counting
+//   the request's keys below it (at most 127 broadcast LDS reads);
+// * one thread per request walks its ordered segment adding path
+//   probabilities in float32 to find how many picks reach its need;
+// * the budget is dealt in descending order of need as a prefix sum: a
+//   request is granted what is left after the wants of every request ranked
+//   before it;
+// * the throughput phase needs only the best `remaining budget` of the
+//   candidates left over (probability descending, depth, request, index):
+//   a radix select over 11-bit digits of the keys, held in registers, finds
+//   the threshold key, stopping as soon as the digit bucket it lands in is
+//   taken whole;
+// * one wave per request numbers the picked candidates by (depth, index)
+//   with ballots and writes the request's output rows.
 // Ties go to the smaller depth, so a node is never picked before its parent
 // and every tree stays connected (appendix: greedy selection is connected).
 #include "device_common.h"
@@ -23,47 +30,43 @@ namespace adaserve {
 namespace {
 
 constexpr int kThreads = 1024;
+constexpr int kPerThread = kSelectMaxCandidates / kThreads;
 constexpr uint64_t kNone = ~0ull;
+constexpr int kDigitBits = 11;
+constexpr int kBins = 1 << kDigitBits;
+constexpr int kTopShift = 44;   // keys are 55 bits: digits at 44, 33, 22, 11, 0
+
+static_assert(kSelectMaxCandidates % kThreads == 0, "candidates per thread");
+static_assert(kSelectMaxRequests <= 512 && kSelectMaxPerRequest <= 127, "key field widths");
+static_assert(kBins * 4 <= kSelectMaxCandidates * 4, "the histogram lives in the probability array");
 
 // A NaN need asks for nothing and ranks last.
 __device__ __forceinline__ float sane_need(float x) { return x != x ? -INFINITY : x; }
 
-__device__ __forceinline__ void bitonic_sort(uint64_t *key, int n) {
-  for (int k = 2; k <= n; k <<= 1)
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = threadIdx.x; i < n; i += kThreads) {
-        const int ixj = i ^ j;
-        if (ixj > i) {
-          const uint64_t a = key[i], b = key[ixj];
-          const bool up = (i & k) == 0;
-          if ((a > b) == up) {
-            key[i] = b;
-            key[ixj] = a;
-          }
-        }
-      }
-      __syncthreads();
-    }
-}
+// ~probability bits: a larger positive float gives a smaller value
+__device__ __forceinline__ uint64_t prob_desc(float p) { return (uint64_t)(~__float_as_uint(p)); }
 
 __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
-  __shared__ uint64_t key[kSelectMaxCandidates];
-  __shared__ float prob[kSelectMaxCandidates];
+  __shared__ uint64_t key[kSelectMaxCandidates];   // request segments, best first
+  __shared__ float prob[kSelectMaxCandidates];     // later the radix histogram
   __shared__ int16_t par[kSelectMaxCandidates];
+  __shared__ uint16_t rq[kSelectMaxCandidates];    // request of each candidate
   __shared__ uint8_t depth[kSelectMaxCandidates];
   __shared__ uint8_t picked[kSelectMaxCandidates];
   __shared__ int32_t lo[kSelectMaxRequests + 1];
   __shared__ int32_t ok[kSelectMaxRequests];
-  __shared__ int32_t seg[kSelectMaxRequests];     // start of the request's sorted segment
-  __shared__ int32_t want[kSelectMaxRequests];    // SLO picks before the budget
-  __shared__ int32_t take[kSelectMaxRequests];    // SLO picks granted
-  __shared__ int32_t order[kSelectMaxRequests];   // requests by descending need
+  __shared__ float need[kSelectMaxRequests];
+  __shared__ int32_t want[kSelectMaxRequests];     // SLO picks before the budget
+  __shared__ int32_t take[kSelectMaxRequests];     // SLO picks granted
   __shared__ int32_t batch_ok, remaining;
+  __shared__ int32_t sel_digit, sel_rank, sel_count, sel_all;
 
   const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
   const int B = a.num_requests, C = a.num_candidates;
   if (tid == 0) batch_ok = 1;
   for (int r = tid; r <= B; r += kThreads) lo[r] = a.cand_indptr[r];
+  for (int r = tid; r < B; r += kThreads) need[r] = sane_need(a.need[r]);
   __syncthreads();
   // the index array must describe exactly the C candidates
   for (int r = tid; r < B; r += kThreads)
@@ -80,23 +83,22 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
     prob[i] = good ? a.cand_prob[i] : 0.f;
     par[i] = good ? (int16_t)max(-2, min(a.cand_parent[i], 32767)) : (int16_t)-2;
     picked[i] = 0;
+    if (good) {   // the r with lo[r] <= i < lo[r + 1] (lo is sorted here)
+      int l = 0, h = B - 1;
+      while (l < h) {
+        const int m = (l + h + 1) >> 1;
+        if (lo[m] <= i) l = m; else h = m - 1;
+      }
+      rq[i] = (uint16_t)l;
+    }
   }
   __syncthreads();
-  auto request_of = [&](int i) {   // the r with lo[r] <= i < lo[r + 1] (lo is sorted here)
-    int l = 0, h = B - 1;
-    while (l < h) {
-      const int m = (l + h + 1) >> 1;
-      if (lo[m] <= i) l = m; else h = m - 1;
-    }
-    return l;
-  };
   if (good)
     for (int i = tid; i < C; i += kThreads) {
-      const int r = request_of(i);
-      const int local = i - lo[r];
+      const int r = rq[i];
       const int p = par[i];
       const float f = prob[i];
-      bool valid = p == -1 || (p >= 0 && p < local);
+      bool valid = p == -1 || (p >= 0 && p < i - lo[r]);
       if (valid) {
         const float fp = p == -1 ? 1.f : prob[lo[r] + p];
         valid = f > 0.f && f <= fp;   // NaN fails
@@ -104,179 +106,238 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
       if (!valid) ok[r] = 0;
     }
   __syncthreads();
-  // depths (a walk up the parents; well-formed requests only)
+  // depths (a walk up the parents) and the request-local keys
   if (good)
     for (int i = tid; i < C; i += kThreads) {
-      const int r = request_of(i);
-      int d = 0;
+      const int r = rq[i];
+      uint64_t k = kNone;
       if (ok[r]) {
-        int v = i - lo[r];
-        while (v >= 0) {
-          ++d;
-          v = par[lo[r] + v];
-        }
+        int d = 0;
+        for (int v = i - lo[r]; v >= 0; v = par[lo[r] + v]) ++d;
+        depth[i] = (uint8_t)d;
+        k = (prob_desc(prob[i]) << 23) | ((uint64_t)d << 16) | ((uint64_t)(i - lo[r]) << 9);
       }
-      depth[i] = (uint8_t)d;
+      key[i] = k;
     }
-  // segment starts: well-formed requests in index order
-  if (tid == 0) {
-    int s = 0;
-    for (int r = 0; r < B; ++r) {
-      seg[r] = s;
-      if (ok[r]) s += lo[r + 1] - lo[r];
-    }
-  }
   __syncthreads();
-  // sort 1, per request: (probability descending, depth, index); one wave
-  // sorts a request's (at most 127) keys in registers, two per lane, with a
-  // bitonic network, and writes them to the request's segment
+
+  // best-first order inside each request: a key's place is the number of the
+  // request's keys below it (keys are distinct: the index is part of them)
   {
-    const int lane = tid & 63, wave = tid >> 6;
-    for (int r = wave; r < B; r += kThreads / 64) {
-      if (!ok[r]) continue;
-      const int nr = lo[r + 1] - lo[r];
-      uint64_t k2[2];
+    uint64_t mine[kPerThread];
+    int place[kPerThread];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int j = lane + 64 * h;
-        const int i = lo[r] + j;
-        k2[h] = j < nr ? ((uint64_t)(~__float_as_uint(prob[i])) << 23) | ((uint64_t)depth[i] << 16) |
-                             ((uint64_t)j << 9)
-                       : kNone;
-      }
-      for (int k = 2; k <= 128; k <<= 1)
-        for (int j = k >> 1; j > 0; j >>= 1) {
-          uint64_t nk[2];
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int e = lane + 64 * h;   // element index; its partner is e ^ j
-            const uint64_t other = j == 64 ? k2[h ^ 1] : (uint64_t)__shfl_xor((unsigned long long)k2[h], j, 64);
-            const bool lower = (e & j) == 0;
-            const bool up = (e & k) == 0;   // ascending block
-            const uint64_t mn = other < k2[h] ? other : k2[h], mx = other < k2[h] ? k2[h] : other;
-            nk[h] = (lower == up) ? mn : mx;
-          }
-          k2[0] = nk[0];
-          k2[1] = nk[1];
-        }
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int j = lane + 64 * h;
-        if (j < nr) key[seg[r] + j] = k2[h];
+    for (int s = 0; s < kPerThread; ++s) {
+      const int i = tid + s * kThreads;
+      mine[s] = kNone;
+      place[s] = 0;
+      if (good && i < C && ok[rq[i]]) {
+        const int r = rq[i];
+        const uint64_t me = key[i];
+        int below = 0;
+#pragma unroll 8
+        for (int q = lo[r]; q < lo[r + 1]; ++q) below += key[q] < me ? 1 : 0;
+        mine[s] = me;
+        place[s] = lo[r] + below;
       }
     }
+    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < kPerThread; ++s)
+      if (mine[s] != kNone) key[place[s]] = mine[s];
   }
   __syncthreads();
 
   // each request's SLO picks: add the best remaining candidate while the
   // float32 sum of the added probabilities is below its need and the tree is
-  // under n_max nodes
+  // under n_max nodes (keys are read four ahead of the running sum)
   for (int r = tid; r < B; r += kThreads) {
     int k = 0;
     if (ok[r]) {
-      const int nr = lo[r + 1] - lo[r];
-      const float need = sane_need(a.need[r]);
+      const int lim = min(lo[r + 1] - lo[r], a.n_max - 1);
+      const float nd = need[r];
+      const uint64_t *seg = key + lo[r];
       float acc = 0.f;
-      while (k < nr && acc < need && 1 + k < a.n_max) {
-        acc += __uint_as_float(~(uint32_t)(key[seg[r] + k] >> 23));
-        ++k;
+      while (k < lim && acc < nd) {
+        float f[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          f[u] = k + u < lim ? __uint_as_float(~(uint32_t)(seg[k + u] >> 23)) : 0.f;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (k < lim && acc < nd) {
+            acc += f[u];
+            ++k;
+          }
       }
     }
     want[r] = k;
   }
-  // requests by descending need, ties by index
+  __syncthreads();
+  // the budget, dealt in descending order of need (ties by index): every
+  // well-formed request keeps its root, then a request gets what is left
+  // after the wants of the requests ranked before it
   for (int r = tid; r < B; r += kThreads) {
-    if (!ok[r]) continue;
-    const float nr = sane_need(a.need[r]);
-    int rank = 0;
+    const float nr = need[r];
+    int valid = 0, ahead = 0, total = 0;
     for (int q = 0; q < B; ++q) {
       if (!ok[q]) continue;
-      const float nq = sane_need(a.need[q]);
-      rank += (nq > nr || (nq == nr && q < r)) ? 1 : 0;
+      const float nq = need[q];
+      const int w = want[q];
+      ++valid;
+      total += w;
+      ahead += (nq > nr || (nq == nr && q < r)) ? w : 0;
     }
-    order[rank] = r;
+    const int left = a.budget - valid;
+    take[r] = ok[r] ? min(want[r], max(left - ahead, 0)) : 0;
+    if (r == 0) remaining = max(left - total, 0);
   }
   __syncthreads();
-  if (tid == 0) {
-    int valid = 0;
-    for (int r = 0; r < B; ++r) {
-      valid += ok[r] ? 1 : 0;
-      take[r] = 0;
-    }
-    int left = a.budget - valid;
-    for (int k = 0; k < valid; ++k) {
-      const int r = order[k];
-      const int t = min(want[r], max(left, 0));
-      take[r] = t;
-      left -= t;
-    }
-    remaining = max(left, 0);
-  }
-  __syncthreads();
-  for (int r = tid; r < B; r += kThreads)
-    for (int k = 0; k < take[r]; ++k) {
-      const int local = (int)((key[seg[r] + k] >> 9) & 0x7f);
-      picked[lo[r] + local] = 1;
+  for (int i = tid; i < C; i += kThreads)
+    if (good) {
+      const int r = rq[i];
+      if (ok[r] && i - lo[r] < take[r]) picked[lo[r] + (int)((key[i] >> 9) & 0x7f)] = 1;
     }
   __syncthreads();
 
-  // sort 2: the remaining candidates of the batch, best first
-  int n = 2;
-  while (n < C) n <<= 1;
-  for (int i = tid; i < n; i += kThreads) {
-    uint64_t k = kNone;
-    if (good && i < C && !picked[i]) {
-      const int r = request_of(i);
-      if (ok[r])
-        k = ((uint64_t)(~__float_as_uint(prob[i])) << 32) | ((uint64_t)depth[i] << 25) |
-            ((uint64_t)r << 16) | (uint64_t)(i - lo[r]);
+  // throughput phase: the best `remaining` of the candidates left, keyed
+  // (probability descending, depth, request, index), found by radix select
+  uint64_t k2[kPerThread];
+#pragma unroll
+  for (int s = 0; s < kPerThread; ++s) {
+    const int i = tid + s * kThreads;
+    k2[s] = kNone;
+    if (good && i < C && ok[rq[i]] && !picked[i]) {
+      const int r = rq[i];
+      k2[s] = (prob_desc(prob[i]) << 23) | ((uint64_t)depth[i] << 16) | ((uint64_t)r << 7) | (uint64_t)(i - lo[r]);
     }
-    key[i] = k;
   }
-  __syncthreads();
-  bitonic_sort(key, n);
-  for (int k = tid; k < remaining && k < n; k += kThreads) {
-    const uint64_t kk = key[k];
-    if (kk == kNone) continue;
-    const int r = (int)((kk >> 16) & 0x1ff), local = (int)(kk & 0x7f);
-    picked[lo[r] + local] = 1;
-  }
-  __syncthreads();
-
-  // output: root first, then the picked candidates by (depth, index)
-  int16_t *tree_id = (int16_t *)key;   // key[] is free now
-  if (good)
-    for (int i = tid; i < C; i += kThreads) {
-      const int r = request_of(i);
-      int16_t t = -1;
-      if (ok[r] && picked[i]) {
-        int before = 0;
-        for (int j = lo[r]; j < lo[r + 1]; ++j)
-          before += (picked[j] && (depth[j] < depth[i] || (depth[j] == depth[i] && j < i))) ? 1 : 0;
-        t = (int16_t)(1 + before);
+  __syncthreads();   // prob[] is the histogram from here on
+  if (remaining > 0) {
+    uint32_t *hist = (uint32_t *)prob;
+    uint64_t prefix = 0;   // the digits chosen so far
+    int want_rank = remaining, shift = kTopShift;
+    for (;; shift -= kDigitBits) {
+      for (int b = tid; b < kBins; b += kThreads) hist[b] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int s = 0; s < kPerThread; ++s)
+        if (k2[s] != kNone && (k2[s] >> (shift + kDigitBits)) == (prefix >> (shift + kDigitBits)))
+          atomicAdd(&hist[(k2[s] >> shift) & (kBins - 1)], 1u);
+      __syncthreads();
+      if (wave == 0) {
+        // lane l holds bins [32 l, 32 l + 32); the bucket holding the
+        // want_rank-th key is where the running count first reaches it
+        uint32_t c[32];
+        const uint4 *h4 = (const uint4 *)(hist + 32 * lane);
+        uint32_t sum = 0;
+#pragma unroll
+        for (int v = 0; v < 8; ++v) {
+          const uint4 x = h4[v];
+          c[4 * v] = x.x;
+          c[4 * v + 1] = x.y;
+          c[4 * v + 2] = x.z;
+          c[4 * v + 3] = x.w;
+          sum += x.x + x.y + x.z + x.w;
+        }
+        uint32_t incl = sum;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const uint32_t y = __shfl_up(incl, o, 64);
+          if (lane >= o) incl += y;
+        }
+        const uint32_t total = __shfl(incl, 63, 64);
+        const uint32_t wr = (uint32_t)want_rank;
+        if (wr > total) {
+          if (lane == 0) sel_all = 1;
+        } else {
+          const unsigned long long hit = __ballot(incl >= wr);
+          if (lane == __ffsll((long long)hit) - 1) {
+            uint32_t cum = incl - sum;
+            int digit = 0;
+            uint32_t cnt = 0;
+            bool found = false;
+#pragma unroll
+            for (int b = 0; b < 32; ++b)
+              if (!found && cum + c[b] >= wr) {
+                found = true;
+                digit = 32 * lane + b;
+                cnt = c[b];
+              } else if (!found) {
+                cum += c[b];
+              }
+            sel_all = 0;
+            sel_digit = digit;
+            sel_rank = (int)(wr - cum);
+            sel_count = (int)cnt;
+          }
+        }
       }
-      tree_id[i] = t;
+      __syncthreads();
+      if (sel_all) {
+        prefix = kNone;   // fewer keys left than budget: take them all
+        break;
+      }
+      prefix |= (uint64_t)sel_digit << shift;
+      want_rank = sel_rank;
+      // a bucket taken whole ends the search; the last digit is one key
+      if (sel_count == want_rank || shift == 0) break;
     }
-  __syncthreads();
-  for (int w = tid; w < B * a.max_nodes; w += kThreads) {
-    a.tree_parent[w] = -1;
-    a.tree_cand[w] = -1;
+#pragma unroll
+    for (int s = 0; s < kPerThread; ++s)
+      if (k2[s] != kNone && (k2[s] >> shift) <= (prefix >> shift)) picked[tid + s * kThreads] = 1;
   }
-  __syncthreads();   // the row fills above happen before the entries below
-  if (good)
-    for (int i = tid; i < C; i += kThreads) {
-      const int t = tree_id[i];
-      if (t < 0) continue;
-      const int r = request_of(i);
-      const int p = par[i];
-      a.tree_cand[(int64_t)r * a.max_nodes + t] = i - lo[r];
-      a.tree_parent[(int64_t)r * a.max_nodes + t] = p == -1 ? 0 : tree_id[lo[r] + p];
+  __syncthreads();
+
+  // output, one wave per request: root first, then the picked candidates by
+  // (depth, index), numbered level by level with ballots
+  const unsigned long long below = (1ull << lane) - 1;
+  for (int r = wave; r < B; r += kThreads / 64) {
+    int32_t *tp = a.tree_parent + (int64_t)r * a.max_nodes;
+    int32_t *tc = a.tree_cand + (int64_t)r * a.max_nodes;
+    if (!ok[r]) {
+      for (int t = lane; t < a.max_nodes; t += 64) {
+        tp[t] = -1;
+        tc[t] = -1;
+      }
+      if (lane == 0) a.tree_size[r] = -1;
+      continue;
     }
-  for (int r = tid; r < B; r += kThreads) {
-    int cnt = 0;
-    if (ok[r])
-      for (int j = lo[r]; j < lo[r + 1]; ++j) cnt += picked[j];
-    a.tree_size[r] = ok[r] ? 1 + cnt : -1;
+    const int base = lo[r], nr = lo[r + 1] - base;
+    bool pk[2];
+    int dp[2], id[2] = {-1, -1};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int e = lane + 64 * h;
+      pk[h] = e < nr && picked[base + e];
+      dp[h] = e < nr ? depth[base + e] : 0;
+    }
+    const int total = __popcll(__ballot(pk[0])) + __popcll(__ballot(pk[1]));
+    int next = 1;
+    for (int d = 1; next <= total && d <= kSelectMaxPerRequest; ++d) {
+      const bool at0 = pk[0] && dp[0] == d, at1 = pk[1] && dp[1] == d;
+      const unsigned long long m0 = __ballot(at0), m1 = __ballot(at1);
+      if (at0) id[0] = next + __popcll(m0 & below);
+      if (at1) id[1] = next + __popcll(m0) + __popcll(m1 & below);
+      next += __popcll(m0) + __popcll(m1);
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int e = lane + 64 * h;
+      const int pp = e < nr ? par[base + e] : -1;
+      const int src = pp < 0 ? 0 : pp;
+      const int x0 = __shfl(id[0], src & 63, 64), x1 = __shfl(id[1], src & 63, 64);
+      if (pk[h] && id[h] > 0) {
+        tc[id[h]] = e;
+        tp[id[h]] = pp < 0 ? 0 : (src < 64 ? x0 : x1);
+      }
+    }
+    for (int t = lane; t < a.max_nodes; t += 64)
+      if (t == 0 || t > total) {
+        tp[t] = -1;
+        tc[t] = -1;
+      }
+    if (lane == 0) a.tree_size[r] = 1 + total;
   }
 }
 

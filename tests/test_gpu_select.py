@@ -80,3 +80,21 @@ def test_select_malformed_and_bad_index_array(torch_cuda):
     bad[-1] += 1
     size, _, _ = _check(torch_cuda, c, indptr=bad)
     assert (size == -1).all()
+
+
+@pytest.mark.parametrize("B,d,w,levels,budget", [
+    (512, 4, 4, 2, "third"),      # 8192 candidates, 512 requests: both limits at once, heavy ties
+    (512, 16, 1, 1, "third"),     # every path probability 1: ranked by depth, request, index alone
+    (64, 127, 1, 1, "third"),     # chains of 127: the deepest trees
+    (8, 1, 127, 1, "third"),      # 127 siblings of probability 1
+    (8, 3, 42, 1, "all"),         # budget beyond every candidate: all are taken
+    (8, 3, 42, 3, "roots"),       # budget of the roots alone: nothing is added
+    (33, 5, 7, None, "third"),
+])
+def test_select_ties_depths_and_limits(torch_cuda, B, d, w, levels, budget):
+    rng = np.random.Generator(np.random.PCG64(B * 1000 + d * 10 + w))
+    c = make_candidates(rng, B, d, w, prob_levels=levels)
+    total = B * (1 + d * w)
+    c.budget = {"third": total // 3, "all": total + 10, "roots": B}[budget]
+    size, _, _ = _check(torch_cuda, c)
+    assert size.sum() == min(c.budget, total)
