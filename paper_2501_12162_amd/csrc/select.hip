@@ -55,8 +55,7 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
   __shared__ uint8_t picked[kSelectMaxCandidates];
   __shared__ int32_t lo[kSelectMaxRequests + 1];
   __shared__ int32_t ok[kSelectMaxRequests];
-  __shared__ float need[kSelectMaxRequests];
-  __shared__ int32_t want[kSelectMaxRequests];     // SLO picks before the budget
+  __shared__ int2 wn[kSelectMaxRequests];          // (SLO picks before the budget or -1, need bits)
   __shared__ int32_t take[kSelectMaxRequests];     // SLO picks granted
   __shared__ int32_t batch_ok, remaining;
   __shared__ int32_t sel_digit, sel_rank, sel_count, sel_all;
@@ -66,7 +65,7 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
   const int B = a.num_requests, C = a.num_candidates;
   if (tid == 0) batch_ok = 1;
   for (int r = tid; r <= B; r += kThreads) lo[r] = a.cand_indptr[r];
-  for (int r = tid; r < B; r += kThreads) need[r] = sane_need(a.need[r]);
+  for (int r = tid; r < B; r += kThreads) wn[r] = make_int2(-1, __float_as_int(sane_need(a.need[r])));
   __syncthreads();
   // the index array must describe exactly the C candidates
   for (int r = tid; r < B; r += kThreads)
@@ -83,15 +82,10 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
     prob[i] = good ? a.cand_prob[i] : 0.f;
     par[i] = good ? (int16_t)max(-2, min(a.cand_parent[i], 32767)) : (int16_t)-2;
     picked[i] = 0;
-    if (good) {   // the r with lo[r] <= i < lo[r + 1] (lo is sorted here)
-      int l = 0, h = B - 1;
-      while (l < h) {
-        const int m = (l + h + 1) >> 1;
-        if (lo[m] <= i) l = m; else h = m - 1;
-      }
-      rq[i] = (uint16_t)l;
-    }
   }
+  if (good)   // the segments of a well-formed index array tile [0, C)
+    for (int r = wave; r < B; r += kThreads / 64)
+      for (int i = lo[r] + lane; i < lo[r + 1]; i += 64) rq[i] = (uint16_t)r;
   __syncthreads();
   if (good)
     for (int i = tid; i < C; i += kThreads) {
@@ -121,30 +115,30 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
     }
   __syncthreads();
 
-  // best-first order inside each request: a key's place is the number of the
-  // request's keys below it (keys are distinct: the index is part of them)
-  {
-    uint64_t mine[kPerThread];
-    int place[kPerThread];
-#pragma unroll
-    for (int s = 0; s < kPerThread; ++s) {
-      const int i = tid + s * kThreads;
-      mine[s] = kNone;
-      place[s] = 0;
-      if (good && i < C && ok[rq[i]]) {
-        const int r = rq[i];
-        const uint64_t me = key[i];
-        int below = 0;
-#pragma unroll 8
-        for (int q = lo[r]; q < lo[r + 1]; ++q) below += key[q] < me ? 1 : 0;
-        mine[s] = me;
-        place[s] = lo[r] + below;
+  // best-first order inside each request, one wave per request: a key's
+  // place is the number of the request's keys below it (keys are distinct:
+  // the index is part of them); the wave reads the whole segment before it
+  // writes it back in order
+  for (int r = wave; r < B; r += kThreads / 64) {
+    if (!ok[r]) continue;
+    const int base = lo[r], nr = lo[r + 1] - base;
+    const uint64_t m0 = lane < nr ? key[base + lane] : kNone;
+    const uint64_t m1 = lane + 64 < nr ? key[base + lane + 64] : kNone;
+    int b0 = 0, b1 = 0;
+    if (nr <= 64) {
+#pragma unroll 4
+      for (int q = 0; q < nr; ++q) b0 += key[base + q] < m0 ? 1 : 0;
+    } else {
+#pragma unroll 4
+      for (int q = 0; q < nr; ++q) {
+        const uint64_t kq = key[base + q];
+        b0 += kq < m0 ? 1 : 0;
+        b1 += kq < m1 ? 1 : 0;
       }
     }
-    __syncthreads();
-#pragma unroll
-    for (int s = 0; s < kPerThread; ++s)
-      if (mine[s] != kNone) key[place[s]] = mine[s];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    if (lane < nr) key[base + b0] = m0;
+    if (lane + 64 < nr) key[base + b1] = m1;
   }
   __syncthreads();
 
@@ -155,7 +149,7 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
     int k = 0;
     if (ok[r]) {
       const int lim = min(lo[r + 1] - lo[r], a.n_max - 1);
-      const float nd = need[r];
+      const float nd = __int_as_float(wn[r].y);
       const uint64_t *seg = key + lo[r];
       float acc = 0.f;
       while (k < lim && acc < nd) {
@@ -171,26 +165,42 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
           }
       }
     }
-    want[r] = k;
+    if (ok[r]) wn[r].x = k;
   }
   __syncthreads();
   // the budget, dealt in descending order of need (ties by index): every
   // well-formed request keeps its root, then a request gets what is left
-  // after the wants of the requests ranked before it
-  for (int r = tid; r < B; r += kThreads) {
-    const float nr = need[r];
+  // after the wants of the requests ranked before it; a group of G lanes
+  // shares each request's pass over the batch
+  {
+    int G = 64;
+    while (G > 1 && G * B > kThreads) G >>= 1;
+    const int r = tid / G, j = tid % G;
     int valid = 0, ahead = 0, total = 0;
-    for (int q = 0; q < B; ++q) {
-      if (!ok[q]) continue;
-      const float nq = need[q];
-      const int w = want[q];
-      ++valid;
-      total += w;
-      ahead += (nq > nr || (nq == nr && q < r)) ? w : 0;
+    int2 me = make_int2(-1, 0);
+    if (r < B) {
+      me = wn[r];
+      const float nr = __int_as_float(me.y);
+#pragma unroll 4
+      for (int q = j; q < B; q += G) {
+        const int2 x = wn[q];
+        const float nq = __int_as_float(x.y);
+        const int w = max(x.x, 0);
+        valid += x.x >= 0 ? 1 : 0;
+        total += w;
+        ahead += (nq > nr || (nq == nr && q < r)) ? w : 0;
+      }
     }
-    const int left = a.budget - valid;
-    take[r] = ok[r] ? min(want[r], max(left - ahead, 0)) : 0;
-    if (r == 0) remaining = max(left - total, 0);
+    for (int o = 1; o < G; o <<= 1) {   // groups are aligned inside a wave
+      valid += __shfl_xor(valid, o, 64);
+      total += __shfl_xor(total, o, 64);
+      ahead += __shfl_xor(ahead, o, 64);
+    }
+    if (r < B && j == 0) {
+      const int left = a.budget - valid;
+      take[r] = me.x >= 0 ? min(me.x, max(left - ahead, 0)) : 0;
+      if (r == 0) remaining = max(left - total, 0);
+    }
   }
   __syncthreads();
   for (int i = tid; i < C; i += kThreads)
