@@ -47,7 +47,7 @@ __device__ __forceinline__ float sane_need(float x) { return x != x ? -INFINITY 
 __device__ __forceinline__ uint64_t prob_desc(float p) { return (uint64_t)(~__float_as_uint(p)); }
 
 __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
-  __shared__ uint64_t key[kSelectMaxCandidates];   // request segments, best first
+  __shared__ __align__(16) uint64_t key[kSelectMaxCandidates];   // request segments, best first
   __shared__ float prob[kSelectMaxCandidates];     // later the radix histogram
   __shared__ int16_t par[kSelectMaxCandidates];
   __shared__ uint16_t rq[kSelectMaxCandidates];    // request of each candidate
@@ -120,22 +120,39 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
   // the index is part of them); the wave reads the whole segment before it
   // writes it back in order
   for (int r = wave; r < B; r += kThreads / 64) {
-    if (!ok[r]) continue;
     const int base = lo[r], nr = lo[r + 1] - base;
+    if (!ok[r] || nr == 0) continue;
     const uint64_t m0 = lane < nr ? key[base + lane] : kNone;
     const uint64_t m1 = lane + 64 < nr ? key[base + lane + 64] : kNone;
-    int b0 = 0, b1 = 0;
+    // keys two at a time from 16-byte-aligned pairs, two counters per key
+    int b0 = 0, b1 = 0, c0 = 0, c1 = 0;
+    const int head = base & 1, pairs = (nr - head) >> 1;
+    const ulonglong2 *kp = (const ulonglong2 *)(key + base + head);
+    if (head) b0 += key[base] < m0 ? 1 : 0, b1 += key[base] < m1 ? 1 : 0;
+    if ((nr - head) & 1) {
+      const uint64_t kq = key[base + nr - 1];
+      c0 += kq < m0 ? 1 : 0;
+      c1 += kq < m1 ? 1 : 0;
+    }
     if (nr <= 64) {
-#pragma unroll 4
-      for (int q = 0; q < nr; ++q) b0 += key[base + q] < m0 ? 1 : 0;
+#pragma unroll 8
+      for (int q = 0; q < pairs; ++q) {
+        const ulonglong2 x = kp[q];
+        b0 += x.x < m0 ? 1 : 0;
+        c0 += x.y < m0 ? 1 : 0;
+      }
     } else {
 #pragma unroll 4
-      for (int q = 0; q < nr; ++q) {
-        const uint64_t kq = key[base + q];
-        b0 += kq < m0 ? 1 : 0;
-        b1 += kq < m1 ? 1 : 0;
+      for (int q = 0; q < pairs; ++q) {
+        const ulonglong2 x = kp[q];
+        b0 += x.x < m0 ? 1 : 0;
+        c0 += x.y < m0 ? 1 : 0;
+        b1 += x.x < m1 ? 1 : 0;
+        c1 += x.y < m1 ? 1 : 0;
       }
     }
+    b0 += c0;
+    b1 += c1;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     if (lane < nr) key[base + b0] = m0;
     if (lane + 64 < nr) key[base + b1] = m1;
