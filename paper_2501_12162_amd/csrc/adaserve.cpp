@@ -109,6 +109,7 @@ struct AttnPlan {
   int32_t rows_per_tile = 0;
   int32_t chunk_target = 0;
   int32_t chunk_floor = 0;
+  std::vector<int32_t> chunk_len;  // prefix keys per unit of each request
   int64_t units = 0;
   int64_t padded_grid = 0;
   int64_t row_groups = 0;
@@ -190,20 +191,20 @@ double lpt_makespan(std::vector<std::pair<double, int64_t>> &units) {
   return runs.back().first;
 }
 
-// Plan for one (chunk target, chunk floor) choice with 128-row tiles.  The
+// Plan for one choice of per-request chunk lengths `ck` (prefix keys per
+// unit, whole 32-key blocks, at most kMaxChunk) with 128-row tiles.  The
 // cost estimate is the larger of the longest-first makespan of the units
-// and the chip-wide streaming time (K/V plus the split partials), plus the
-// combine pass when a prefix is split.  evaluate_plan fills everything but
+// and the chip-wide streaming time (K/V plus the split partials, at a rate
+// scaled by the share of workgroup slots the units fill), plus the combine
+// pass when a prefix is split.  evaluate_plan fills everything but
 // the makespan and returns the unit list; `bound` is a lower bound of the
 // estimate (the makespan replaced by max(longest unit, total / slots)).
 AttnPlan evaluate_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
-                       int32_t group, int32_t head_dim, int32_t rows_per_tile, int32_t chunk_target,
-                       int32_t floor_mult, std::vector<std::pair<double, int64_t>> &units, double &fixed,
-                       double &bound) {
+                       int32_t group, int32_t head_dim, int32_t rows_per_tile, const std::vector<int32_t> &ck,
+                       std::vector<std::pair<double, int64_t>> &units, double &fixed, double &bound) {
   AttnPlan p;
   p.rows_per_tile = rows_per_tile;
-  p.chunk_target = chunk_target;
-  p.chunk_floor = floor_mult;
+  p.chunk_len = ck;
   const double key_bytes = 4.0 * head_dim;  // bf16 K and V of one key of one kv-head
   double kv_bytes = 0, partial_bytes = 0, total = 0;
   units.clear();
@@ -211,8 +212,7 @@ AttnPlan evaluate_plan(int32_t B, const int32_t *indptr_host, const int32_t *ple
     const int32_t n = indptr_host[r + 1] - indptr_host[r];
     const int32_t L = plen_host[r];
     const int32_t tiles = row_tiles(n, group, rows_per_tile);
-    const int32_t ck = chunk_keys(n, group, rows_per_tile, chunk_target, floor_mult);
-    const int32_t chunks = prefix_chunks(L, ck);
+    const int32_t chunks = prefix_chunks(L, ck[r]);
     const int64_t cnt = (int64_t)hkv * tiles * chunks;
     p.units += cnt;
     p.row_groups += (int64_t)hkv * tiles;
@@ -222,13 +222,15 @@ AttnPlan evaluate_plan(int32_t B, const int32_t *indptr_host, const int32_t *ple
       partial_bytes += hkv * chunks * n * group * (head_dim * 2.0 + 8.0);
     }
     // every chunk pays the fixed cost; the tree block is spread over them
-    const double blocks = ceil_div(std::min(L, ck), 32) + (double)ceil_div(n, 32) / chunks;
+    const double blocks = ceil_div(std::min(L, ck[r]), 32) + (double)ceil_div(n, 32) / chunks;
     units.push_back({kUnitFixedUs + blocks * kBlockUs, cnt});
     total += units.back().first * cnt;
   }
   double longest = 0;
   for (const auto &u : units) longest = std::max(longest, u.first);
-  const double stream = (kv_bytes + partial_bytes) / kChipBytesPerUs;
+  // the chip streams at full rate only with every workgroup slot busy
+  const double occupancy = std::min(1.0, (double)p.units / kSlots);
+  const double stream = (kv_bytes + partial_bytes) / (kChipBytesPerUs * occupancy);
   const double combine = p.needs_combine ? kCombineUs + partial_bytes / kChipBytesPerUs : 0.0;
   fixed = combine;
   p.est_us = std::max(stream, 0.0);  // completed with the makespan by make_plan
@@ -243,14 +245,19 @@ AttnPlan evaluate_plan(int32_t B, const int32_t *indptr_host, const int32_t *ple
 }
 
 // Work plan of the bf16 kernel, from host-visible sizes only: the cheapest
-// estimate over chunk targets {256 .. 8192} and chunk floors {8, 16, 32}
-// keys per row (see evaluate_plan), 128-row tiles.  (A 64-row tile makes
-// two units read the same K/V for about the same step time, so it never
-// wins.)  Choices that give every request the same chunk length as one
-// already tried are skipped, and the makespan is only simulated for
-// choices whose lower bound can still beat the best estimate so far.
-// Requests are then dispatched in descending order of per-unit cost
-// (fill_plan_table).
+// estimate over two families of prefix splits, 128-row tiles.  (A 64-row
+// tile costs about as much per step as a 128-row one, so it never wins.)
+//  * batch-wide chunk targets {256 .. 8192} with chunk floors {8, 16, 32}
+//    keys per row (chunk_keys() in plan.h), the only family the device can
+//    rebuild without a plan table;
+//  * with a plan table, balanced splits: for a target unit count, every
+//    request's prefix is cut into the fewest equal runs of whole 32-key
+//    blocks no longer than the batch's mean blocks per unit, so the units
+//    come out about equally long and fill the workgroup slots evenly.
+// Choices that give every request the same chunk lengths as one already
+// tried are skipped, and the makespan is only simulated for choices whose
+// lower bound can still beat the best estimate so far.  Requests are then
+// dispatched in descending order of per-unit cost (fill_plan_table).
 AttnPlan make_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
                    int32_t group, int32_t head_dim, int32_t dtype) {
   AttnPlan best;
@@ -258,34 +265,56 @@ AttnPlan make_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_ho
   const int32_t rt = kMaxRowsPerTile;
   struct Cand {
     double bound;
-    int32_t fm, c;
+    int32_t fm, c;   // batch-wide family (fm = 0: balanced)
+    std::vector<int32_t> ck;
   };
   std::vector<Cand> cands;
-  std::vector<std::vector<int32_t>> seen;
-  std::vector<int32_t> cks(B);
   std::vector<std::pair<double, int64_t>> units;
   double fixed, bound;
+  auto add = [&](int32_t fm, int32_t c, std::vector<int32_t> ck) {
+    for (const Cand &x : cands)
+      if (x.ck == ck) return;
+    evaluate_plan(B, indptr_host, plen_host, hkv, group, head_dim, rt, ck, units, fixed, bound);
+    cands.push_back({bound, fm, c, std::move(ck)});
+  };
+  std::vector<int32_t> ck(B);
   for (int32_t fm : {32, 16, 8})
     for (int32_t c = kMaxChunk; c >= kMinChunk; c /= 2) {
-      for (int32_t r = 0; r < B; ++r) {
-        const int32_t n = indptr_host[r + 1] - indptr_host[r];
-        const int32_t ck = chunk_keys(n, group, rt, c, fm);
-        cks[r] = prefix_chunks(plen_host[r], ck) > 1 ? ck : 0;  // 0: unsplit
-      }
-      if (std::find(seen.begin(), seen.end(), cks) != seen.end()) continue;
-      seen.push_back(cks);
-      evaluate_plan(B, indptr_host, plen_host, hkv, group, head_dim, rt, c, fm, units, fixed, bound);
-      cands.push_back({bound, fm, c});
+      for (int32_t r = 0; r < B; ++r) ck[r] = chunk_keys(indptr_host[r + 1] - indptr_host[r], group, rt, c, fm);
+      add(fm, c, ck);
     }
+  if (B <= kPlanMax) {
+    int64_t work = 0;   // unit-blocks of the unsplit batch
+    for (int32_t r = 0; r < B; ++r)
+      work += (int64_t)hkv * row_tiles(indptr_host[r + 1] - indptr_host[r], group, rt) *
+              std::max(1, ceil_div(plen_host[r], kKeysPerBlock));
+    for (int32_t target : {256, 320, 384, 448, 512, 576, 640, 768, 1024}) {
+      const int64_t per_unit = std::max<int64_t>(4, (work + target - 1) / target);
+      for (int32_t r = 0; r < B; ++r) {
+        const int32_t blocks = ceil_div(std::max(plen_host[r], 0), kKeysPerBlock);
+        if (blocks == 0) {
+          ck[r] = kMaxChunk;
+          continue;
+        }
+        const int32_t runs = (int32_t)std::max<int64_t>((blocks + per_unit - 1) / per_unit,
+                                                        ceil_div(blocks, kMaxChunk / kKeysPerBlock));
+        ck[r] = ceil_div(blocks, runs) * kKeysPerBlock;
+      }
+      add(0, 0, ck);
+    }
+  }
   // candidates in the order they were generated break ties (larger chunks first)
   std::stable_sort(cands.begin(), cands.end(), [](const Cand &x, const Cand &y) { return x.bound < y.bound; });
   bool have = false;
   for (const Cand &cd : cands) {
     if (have && cd.bound >= best.est_us * 0.98) break;
-    AttnPlan p = evaluate_plan(B, indptr_host, plen_host, hkv, group, head_dim, rt, cd.c, cd.fm, units, fixed, bound);
+    AttnPlan p = evaluate_plan(B, indptr_host, plen_host, hkv, group, head_dim, rt, cd.ck, units, fixed, bound);
     p.est_us = std::max(p.est_us, lpt_makespan(units)) + fixed;
+    // the batch-wide fields rebuild the chunks when there is no plan table
+    p.chunk_target = cd.fm ? cd.c : kMaxChunk;
+    p.chunk_floor = cd.fm ? cd.fm : 32;
     if (!have || p.est_us < best.est_us * 0.98) {
-      best = p;
+      best = std::move(p);
       have = true;
     }
   }
@@ -302,8 +331,7 @@ void fill_plan_table(TreeAttnArgs &a, int32_t B, const int32_t *indptr_host, con
   int64_t cost[kPlanMax];
   for (int32_t r = 0; r < B; ++r) {
     const int32_t n = indptr_host[r + 1] - indptr_host[r];
-    const int32_t keys = std::min(std::max(plen_host[r], 0),
-                                  chunk_keys(n, a.group, p.rows_per_tile, p.chunk_target, p.chunk_floor));
+    const int32_t keys = std::min(std::max(plen_host[r], 0), p.chunk_len[r]);
     cost[r] = keys + n;  // steps per unit (the step time hardly depends on the row count)
     order[r] = r;
   }
@@ -312,12 +340,12 @@ void fill_plan_table(TreeAttnArgs &a, int32_t B, const int32_t *indptr_host, con
   for (int32_t i = 0; i < B; ++i) {
     const int32_t r = order[i];
     const int32_t n = indptr_host[r + 1] - indptr_host[r];
-    end += request_units(n, plen_host[r], a.num_kv_heads, a.group, p.rows_per_tile, p.chunk_target,
-                         p.chunk_floor);
+    end += (int64_t)a.num_kv_heads * row_tiles(n, a.group, p.rows_per_tile) *
+           prefix_chunks(plen_host[r], p.chunk_len[r]);
     gend += (int64_t)a.num_kv_heads * row_tiles(n, a.group, p.rows_per_tile);
     a.plan[i].unit_end = (int32_t)end;
     a.plan[i].group_end = (int32_t)gend;
-    a.plan[i].request = r;
+    a.plan[i].request_and_chunk = r | ((p.chunk_len[r] / kKeysPerBlock) << 16);
     a.plan[i].node_base = indptr_host[r];
     a.plan[i].n_and_len = n | (plen_host[r] << 8);
   }

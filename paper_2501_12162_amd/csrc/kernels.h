@@ -13,7 +13,7 @@ constexpr int kPlanMax = 160;
 struct PlanEntry {
   int32_t unit_end;   // exclusive end of this request's units in dispatch order
   int32_t group_end;  // exclusive end of its (kv-head, row tile) groups, same order
-  int32_t request;
+  int32_t request_and_chunk;  // request (bits 0..15) | prefix keys per unit / 32 << 16
   int32_t node_base;  // node_indptr[request]
   int32_t n_and_len;  // tree nodes (bits 0..7) | prefix length << 8
 };
@@ -40,8 +40,8 @@ struct TreeAttnArgs {
   int32_t num_kv_heads;
   int32_t group;               // Hq / Hkv
   int32_t rows_per_tile;       // 64 or 128
-  int32_t chunk_target;        // batch-wide prefix chunk (see chunk_keys() in plan.h)
-  int32_t chunk_floor;         // minimum chunk, in keys per tile row
+  int32_t chunk_target;        // batch-wide prefix chunk (chunk_keys() in plan.h), used when
+  int32_t chunk_floor;         // minimum chunk in keys per tile row       plan_count == 0
   int64_t units;               // work units in the batch
   int64_t padded_grid;         // units rounded up to the XCD count
   int64_t row_groups;          // sum over requests of Hkv * row tiles

@@ -3,16 +3,19 @@
 // One work unit = (request r, kv-head g, row tile, prefix chunk).  The rows
 // of (r, g) are the N_r * G (node, q-head-in-group) pairs, row m = node *
 // G + head-in-group, cut into tiles of `rows_per_tile` rows (64 or 128).
-// The prefix of r is cut into chunks of chunk_keys(r) keys; a request with
-// an empty prefix still has one (empty) chunk.  The last chunk of every
-// (r, g, tile) also takes the request's tree block, so every row sees each
-// visible key exactly once.
+// The prefix of r is cut into chunks of whole 32-key blocks, at most
+// kMaxChunk keys each: the chunk length of each request comes from the plan
+// table in the kernel arguments, or, for batches too large for the table,
+// from chunk_keys() below.  A request with an empty prefix still has one
+// (empty) chunk.  The last chunk of every (r, g, tile) also takes the
+// request's tree block, so every row sees each visible key exactly once.
 //
-// A split prefix costs fp32 partial results: per unit, rows * D * 4 bytes
-// written and read back against chunk * D * 4 bytes of bf16 K and V
-// streamed, i.e. a traffic ratio of about 2 * rows / chunk.  chunk_keys()
-// therefore never goes below `floor_mult` * rows keys (the planner picks 8,
-// 16 or 32); above that floor the batch-wide `chunk_target` sets the split.
+// A split prefix costs partial results: per unit, rows * (2 D + 8) bytes
+// (a bf16 output row, an fp32 max and denominator) written and read back
+// against chunk * D * 4 bytes of bf16 K and V streamed, i.e. a traffic
+// ratio of about rows / chunk.  chunk_keys() therefore never goes below
+// `floor_mult` * rows keys (the planner picks 8, 16 or 32); above that
+// floor the batch-wide `chunk_target` sets the split.
 //
 // Units are numbered request by request; inside a request the order is
 // (chunk, g, tile) with the tile fastest, so the tiles that read the same KV

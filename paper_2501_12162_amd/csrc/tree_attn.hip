@@ -188,13 +188,14 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
 
   const int64_t uid = xcd_swizzle(blockIdx.x, a.padded_grid);
   if (uid >= a.units) return;
-  int32_t r, node_base, n, L;
+  int32_t r, node_base, n, L, chunk_len;
   int64_t ubase;
   if (a.plan_count > 0) {
     // the dispatch-ordered plan in the kernel arguments
     const int lo = __builtin_amdgcn_readfirstlane(find_plan_entry(a, uid, false));
     if (lo < 0) return;
-    r = a.plan[lo].request;
+    r = a.plan[lo].request_and_chunk & 0xffff;
+    chunk_len = (a.plan[lo].request_and_chunk >> 16) * kKeysPerBlock;
     ubase = lo > 0 ? a.plan[lo - 1].unit_end : 0;
     node_base = a.plan[lo].node_base;
     n = a.plan[lo].n_and_len & 0xff;
@@ -205,21 +206,24 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
     node_base = a.node_indptr[r];
     n = min(max(a.node_indptr[r + 1] - node_base, 0), kMaxTreeNodes);
     L = max(a.prefix_len[r], 0);
+    chunk_len = chunk_keys(n, a.group, a.rows_per_tile, a.chunk_target, a.chunk_floor);
   }
   // Request values are uniform; make that visible so branches on them stay scalar.
   r = __builtin_amdgcn_readfirstlane(r);
   node_base = __builtin_amdgcn_readfirstlane(node_base);
   n = __builtin_amdgcn_readfirstlane(n);
   L = __builtin_amdgcn_readfirstlane(L);
+  chunk_len = __builtin_amdgcn_readfirstlane(chunk_len);
   ubase = ((int64_t)__builtin_amdgcn_readfirstlane((int32_t)(ubase >> 32)) << 32) |
           (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)ubase);
   if (n == 0 || node_base < 0 || node_base + n > a.total_nodes) return;
+  // a chunk is whole 32-key blocks and its page ids fit the page-id registers
+  if (chunk_len <= 0 || chunk_len > kMaxChunk || chunk_len % kKeysPerBlock != 0) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = a.group;
   const int RT = a.rows_per_tile;
   const int32_t tiles = row_tiles(n, G, RT);
-  const int32_t chunk_len = chunk_keys(n, G, RT, a.chunk_target, a.chunk_floor);
   const int32_t chunks = prefix_chunks(L, chunk_len);
   const int64_t u = uid - ubase;
   const int32_t tile = (int32_t)(u % tiles);
@@ -654,7 +658,8 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
 // Finds the request of (kv-head, row tile) group `gid` from the plan in the
 // kernel arguments, or by scanning the device arrays.
 __device__ __forceinline__ bool group_request(const TreeAttnArgs &a, int64_t gid, int32_t &node_base,
-                                              int32_t &n, int32_t &L, int64_t &ubase, int64_t &gbase) {
+                                              int32_t &n, int32_t &L, int32_t &chunk_len, int64_t &ubase,
+                                              int64_t &gbase) {
   if (a.plan_count > 0) {
     const int lo = __builtin_amdgcn_readfirstlane(find_plan_entry(a, gid, true));
     if (lo < 0) return false;
@@ -663,6 +668,7 @@ __device__ __forceinline__ bool group_request(const TreeAttnArgs &a, int64_t gid
     node_base = a.plan[lo].node_base;
     n = a.plan[lo].n_and_len & 0xff;
     L = a.plan[lo].n_and_len >> 8;
+    chunk_len = (a.plan[lo].request_and_chunk >> 16) * kKeysPerBlock;
     return true;
   }
   int32_t r;
@@ -670,6 +676,7 @@ __device__ __forceinline__ bool group_request(const TreeAttnArgs &a, int64_t gid
   node_base = a.node_indptr[r];
   n = min(max(a.node_indptr[r + 1] - node_base, 0), kMaxTreeNodes);
   L = max(a.prefix_len[r], 0);
+  chunk_len = chunk_keys(n, a.group, a.rows_per_tile, a.chunk_target, a.chunk_floor);
   return true;
 }
 
@@ -685,13 +692,14 @@ __global__ __launch_bounds__(kThreads) void tree_attn_combine_kernel(TreeAttnArg
   const int64_t gid = blockIdx.x / (kMaxRowsPerTile / kRowsPerWg);
   const int rblk = blockIdx.x % (kMaxRowsPerTile / kRowsPerWg);
   if (gid >= a.row_groups) return;
-  int32_t node_base, n, L;
+  int32_t node_base, n, L, chunk_len;
   int64_t ubase, gbase;
-  if (!group_request(a, gid, node_base, n, L, ubase, gbase)) return;
+  if (!group_request(a, gid, node_base, n, L, chunk_len, ubase, gbase)) return;
   if (n == 0 || node_base < 0 || node_base + n > a.total_nodes) return;
+  if (chunk_len <= 0 || chunk_len > kMaxChunk || chunk_len % kKeysPerBlock != 0) return;
   const int G = a.group, RT = a.rows_per_tile;
   const int32_t tiles = row_tiles(n, G, RT);
-  const int32_t chunks = prefix_chunks(L, chunk_keys(n, G, RT, a.chunk_target, a.chunk_floor));
+  const int32_t chunks = prefix_chunks(L, chunk_len);
   if (chunks == 1) return;
   const int64_t u = gid - gbase;
   const int32_t tile = (int32_t)(u % tiles);
