@@ -103,6 +103,22 @@ def test_ragged_tiles_chunks_and_tails(torch_cuda, dtype, head_dim, hq, hkv):
     check_argmax_accept(b, amax, alen, tok, nodes)
 
 
+def test_balanced_splits_with_uneven_prefixes(torch_cuda):
+    """Llama-3-8B head shapes with prefix lengths on every side of the block,
+    page and chunk sizes (0 .. 17000, past the 8192-key chunk cap), so the
+    planner cuts each request's prefix into its own chunk length."""
+    rng = np.random.Generator(np.random.PCG64(57))
+    lens = [0, 1, 31, 32, 33, 300, 1000, 1024, 1025, 2047, 3000, 4096, 5000, 8192, 8193, 17000]
+    sizes = [1, 128, 64, 7, 40, 2, 33, 128, 16, 64, 9, 100, 50, 31, 80, 20]
+    parents = [random_tree(rng, n, 8) for n in sizes]
+    b = make_batch(parents=parents, prefix_lens=lens, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                   dtype="bf16", vocab=1000, seed=57)
+    d, (out, amax, alen, tok, nodes) = run_device(b)
+    assert d.workspace_bytes > 0
+    check_attention(b, out, sample_nodes(b))
+    check_argmax_accept(b, amax, alen, tok, nodes)
+
+
 def test_mask_discriminating_case(torch_cuda):
     rng = np.random.Generator(np.random.PCG64(41))
     parents = [random_tree(rng, 96, 8), random_tree(rng, 40)]
