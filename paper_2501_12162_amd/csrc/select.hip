@@ -128,7 +128,11 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
     int b0 = 0, b1 = 0, c0 = 0, c1 = 0;
     const int head = base & 1, pairs = (nr - head) >> 1;
     const ulonglong2 *kp = (const ulonglong2 *)(key + base + head);
-    if (head) b0 += key[base] < m0 ? 1 : 0, b1 += key[base] < m1 ? 1 : 0;
+    if (head) {
+      const uint64_t kq = key[base];
+      b0 += kq < m0 ? 1 : 0;
+      b1 += kq < m1 ? 1 : 0;
+    }
     if ((nr - head) & 1) {
       const uint64_t kq = key[base + nr - 1];
       c0 += kq < m0 ? 1 : 0;
@@ -153,7 +157,7 @@ __global__ __launch_bounds__(kThreads) void select_trees_kernel(SelectArgs a) {
     }
     b0 += c0;
     b1 += c1;
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");   // every read above precedes the writes
     if (lane < nr) key[base + b0] = m0;
     if (lane + 64 < nr) key[base + b1] = m1;
   }
