@@ -26,7 +26,7 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense
 FP32_PEAK_TFLOPS = 157.3
 METRIC = "verified tree tokens/sec + % peak HBM GB/s, tree-verify attention, 1 MI355X"
 MALL_BYTES = 256 << 20
-EVENT_EVERY = 5                 # one timed step in EVENT_EVERY carries per-kernel events
+EVENT_EVERY = 5                 # the last 1/EVENT_EVERY of the timed steps carry per-kernel events
 
 
 def parse_args():
