@@ -119,6 +119,46 @@ def test_balanced_splits_with_uneven_prefixes(torch_cuda):
     check_argmax_accept(b, amax, alen, tok, nodes)
 
 
+def test_verification_step_replayed_from_a_graph(torch_cuda):
+    """The whole step (attention with its split-KV merge, argmax, acceptance)
+    captured once in a HIP graph, as a serving loop replays it: every replay
+    reproduces the eager outputs bit for bit, with eager steps between the
+    replays and the outputs poisoned before each."""
+    from paper_2501_12162_amd.device import DeviceBatch
+    torch = torch_cuda
+    b = cached_config(2)
+    d = DeviceBatch(b, max_accept=16)
+    assert d.workspace_bytes > 0           # the plan splits prefixes: the merge kernel runs too
+    d.step()
+    torch.cuda.synchronize()
+    outs = (d.out, d.target_argmax, d.accept_len, d.accept_tokens, d.accept_nodes)
+    eager = [t.clone() for t in outs]
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        d.step(stream=s)   # warm-up on the side stream before capture
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        d.step(stream=torch.cuda.current_stream())
+    for rep in range(4):
+        d.out.fill_(float("nan"))
+        for t in outs[1:]:
+            t.fill_(-5)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for got, ref in zip(outs, eager):
+            assert torch.equal(got.view(torch.int16) if got.dtype == torch.bfloat16 else got,
+                               ref.view(torch.int16) if ref.dtype == torch.bfloat16 else ref), rep
+        d.step()   # eager work between replays
+        torch.cuda.synchronize()
+    out, amax, alen, tok, nodes = d.results()
+    check_attention(b, out, sample_nodes(b))
+    check_argmax_accept(b, amax, alen, tok, nodes, max_accept=16)
+
+
 def test_mask_discriminating_case(torch_cuda):
     rng = np.random.Generator(np.random.PCG64(41))
     parents = [random_tree(rng, 96, 8), random_tree(rng, 40)]
