@@ -568,15 +568,34 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   // scores of block j+1 and the PV product of block j; the scores of block
   // j+1 are masked (when they need it) and reduced last, while the PV
   // products run on the matrix cores.
-  auto step = [&](int j, int cs, auto masked, auto has_next) {
+  // `issue` for a block known to be a whole prefix block: no block-kind or
+  // row-count branches, and a page outside the pool sends every lane to the
+  // zero line (base = zero line, offset 0) without a branch.  Steps whose two
+  // fetches are such blocks (most of a long chunk) take this form; it cuts
+  // the scalar work of a step by about a third.
+  auto issue_full = [&](const void *pool, char *dst, int32_t page) {
+    const int32_t p = __builtin_amdgcn_readfirstlane(page);
+    const uint32_t lds = lds_addr(dst) + wave * WI * 1024;
+    const bool ok = p >= 0;
+    const char *base = ok ? (const char *)pool + head_off_b + (int64_t)p * page_stride_b : (const char *)a.zero16;
+#pragma unroll
+    for (int i = 0; i < WI; ++i) dma16_off(base, ok ? page_off[i] : 0u, lds + i * 1024);
+  };
+  auto step = [&](int j, int cs, auto masked, auto has_next, auto full_fetch) {
     constexpr bool kMasked = decltype(masked)::value;
     constexpr bool kNext = decltype(has_next)::value;
+    constexpr bool kFull = decltype(full_fetch)::value;
     const char *cur = ring + cs * (2 * BLK);
     if constexpr (kNext) {
       wait_loads_barrier<6 * WI>();
       char *fill = ring + (cs == 0 ? NST - 1 : cs - 1) * (2 * BLK);
-      issue_k(fill, j + 5, pg5);
-      issue_v(fill, j + 4, pg4);
+      if constexpr (kFull) {
+        issue_full(a.k_pages, fill, pg5);
+        issue_full(a.v_pages, fill + BLK, pg4);
+      } else {
+        issue_k(fill, j + 5, pg5);
+        issue_v(fill, j + 4, pg4);
+      }
       pg4 = pg5;
       pg5 = page_of(j + 6);
     } else {
@@ -606,9 +625,20 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   using No = std::false_type;
   int j = 0, cs = 0;
   auto next_stage = [](int c) { return c == NST - 1 ? 0 : c + 1; };
-  for (; j + 1 < n_full; ++j, cs = next_stage(cs)) step(j, cs, No{}, Yes{});  // block j+1: full prefix block
-  for (; j + 1 < nb; ++j, cs = next_stage(cs)) step(j, cs, Yes{}, Yes{});     // block j+1 needs the mask
-  if (nb > 0) step(nb - 1, cs, No{}, No{});
+  // Blocks j+4 and j+5 whole prefix blocks: five steps per iteration (one
+  // per ring stage, starting at stage 0), so every LDS address of a step is
+  // a constant and folds into the instruction's offset.
+  for (; j + 9 < n_full; j += 5) {
+    step(j, 0, No{}, Yes{}, Yes{});
+    step(j + 1, 1, No{}, Yes{}, Yes{});
+    step(j + 2, 2, No{}, Yes{}, Yes{});
+    step(j + 3, 3, No{}, Yes{}, Yes{});
+    step(j + 4, 4, No{}, Yes{}, Yes{});
+  }
+  for (; j + 5 < n_full; ++j, cs = next_stage(cs)) step(j, cs, No{}, Yes{}, Yes{});
+  for (; j + 1 < n_full; ++j, cs = next_stage(cs)) step(j, cs, No{}, Yes{}, No{});  // block j+1: full prefix block
+  for (; j + 1 < nb; ++j, cs = next_stage(cs)) step(j, cs, Yes{}, Yes{}, No{});     // block j+1 needs the mask
+  if (nb > 0) step(nb - 1, cs, No{}, No{}, No{});
 
   const int q4 = q * 4;
   const float l_tot[2] = {osum[0][0], osum[1][0]};
