@@ -119,6 +119,42 @@ def test_balanced_splits_with_uneven_prefixes(torch_cuda):
     check_argmax_accept(b, amax, alen, tok, nodes)
 
 
+def test_out_of_pool_pages_read_as_zero_pages(torch_cuda):
+    """Block-table entries outside [0, num_pages) -- negative or past the pool
+    -- act as all-zero pages: the call equals, bit for bit, the same batch
+    whose entries point at a real zero page appended to the pool, and the
+    oracle checks that batch.  The entries sit in the start-up blocks, inside
+    long runs of whole prefix blocks (the steady-state fetch path), on both
+    pages of one block, and in the partial last page."""
+    import dataclasses
+    rng = np.random.Generator(np.random.PCG64(71))
+    lens = [5000, 3001, 700, 40]
+    sizes = [128, 20, 64, 5]
+    parents = [random_tree(rng, n, 8) for n in sizes]
+    b = make_batch(parents=parents, prefix_lens=lens, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                   dtype="bf16", vocab=1000, seed=71)
+    P = b.num_pages
+    bad, zero = b.block_table.copy(), b.block_table.copy()
+    marked = 0
+    for r, L in enumerate(lens):
+        npg = -(-L // 16)
+        for k, e in enumerate(sorted({0, 7, 40, 41, 100, npg // 2, npg // 2 + 1, npg - 1})):
+            if e < npg:
+                bad[r, e] = -1 if k % 2 == 0 else P + 3
+                zero[r, e] = P
+                marked += 1
+    assert marked >= 20
+    zpage = np.zeros((1,) + b.k_pages.shape[1:], dtype=b.k_pages.dtype)
+    b_bad = dataclasses.replace(b, block_table=bad)
+    b_zero = dataclasses.replace(b, block_table=zero, k_pages=np.concatenate([b.k_pages, zpage]),
+                                 v_pages=np.concatenate([b.v_pages, zpage]))
+    d, (out_bad, *_) = run_device(b_bad)
+    assert d.workspace_bytes > 0
+    _, (out_zero, *_) = run_device(b_zero)
+    np.testing.assert_array_equal(out_bad, out_zero)
+    check_attention(b_zero, out_zero, sample_nodes(b_zero))
+
+
 def test_verification_step_replayed_from_a_graph(torch_cuda):
     """The whole step (attention with its split-KV merge, argmax, acceptance)
     captured once in a HIP graph, as a serving loop replays it: every replay
