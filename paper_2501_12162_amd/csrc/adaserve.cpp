@@ -342,7 +342,8 @@ void fill_plan_table(TreeAttnArgs &a, int32_t B, const int32_t *indptr_host, con
     const int32_t n = indptr_host[r + 1] - indptr_host[r];
     end += (int64_t)a.num_kv_heads * row_tiles(n, a.group, p.rows_per_tile) *
            prefix_chunks(plen_host[r], p.chunk_len[r]);
-    gend += (int64_t)a.num_kv_heads * row_tiles(n, a.group, p.rows_per_tile);
+    // merge blocks: 16 rows of one kv-head each, for split requests only
+    if (prefix_chunks(plen_host[r], p.chunk_len[r]) > 1) gend += (int64_t)a.num_kv_heads * ceil_div(n * a.group, 16);
     a.plan[i].unit_end = (int32_t)end;
     a.plan[i].group_end = (int32_t)gend;
     a.plan[i].request_and_chunk = r | ((p.chunk_len[r] / kKeysPerBlock) << 16);
@@ -350,6 +351,7 @@ void fill_plan_table(TreeAttnArgs &a, int32_t B, const int32_t *indptr_host, con
     a.plan[i].n_and_len = n | (plen_host[r] << 8);
   }
   a.plan_count = B;
+  a.merge_blocks = gend;
 }
 
 }  // namespace
@@ -458,10 +460,11 @@ int32_t adaserve_tree_attn_verify(int32_t num_requests, const int32_t *node_indp
   a.rows_per_tile = plan.rows_per_tile;
   a.chunk_target = plan.chunk_target;
   a.chunk_floor = plan.chunk_floor;
-  if (dtype == ADASERVE_BF16) fill_plan_table(a, num_requests, node_indptr_host, prefix_len_host, plan);
   a.units = plan.units;
   a.padded_grid = plan.padded_grid;
   a.row_groups = plan.row_groups;
+  a.merge_blocks = plan.row_groups * (kMaxRowsPerTile / 16);
+  if (dtype == ADASERVE_BF16) fill_plan_table(a, num_requests, node_indptr_host, prefix_len_host, plan);
   a.sm_scale = sm_scale;
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   hipStream_t s = (hipStream_t)stream;

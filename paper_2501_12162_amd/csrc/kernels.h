@@ -12,7 +12,7 @@ namespace adaserve {
 constexpr int kPlanMax = 160;
 struct PlanEntry {
   int32_t unit_end;   // exclusive end of this request's units in dispatch order
-  int32_t group_end;  // exclusive end of its (kv-head, row tile) groups, same order
+  int32_t group_end;  // exclusive end of its 16-row merge blocks, same order (none when unsplit)
   int32_t request_and_chunk;  // request (bits 0..15) | prefix keys per unit / 32 << 16
   int32_t node_base;  // node_indptr[request]
   int32_t n_and_len;  // tree nodes (bits 0..7) | prefix length << 8
@@ -45,6 +45,7 @@ struct TreeAttnArgs {
   int64_t units;               // work units in the batch
   int64_t padded_grid;         // units rounded up to the XCD count
   int64_t row_groups;          // sum over requests of Hkv * row tiles
+  int64_t merge_blocks;        // workgroups of the split-KV merge
   float sm_scale;
   float scale_log2;            // sm_scale * log2(e)
   int32_t plan_count;          // entries used in plan[] (0: scan the device arrays)

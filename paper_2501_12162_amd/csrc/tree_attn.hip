@@ -685,58 +685,64 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   }
 }
 
-// Finds the request of (kv-head, row tile) group `gid` from the plan in the
-// kernel arguments, or by scanning the device arrays.
-__device__ __forceinline__ bool group_request(const TreeAttnArgs &a, int64_t gid, int32_t &node_base,
-                                              int32_t &n, int32_t &L, int32_t &chunk_len, int64_t &ubase,
-                                              int64_t &gbase) {
-  if (a.plan_count > 0) {
-    const int lo = __builtin_amdgcn_readfirstlane(find_plan_entry(a, gid, true));
-    if (lo < 0) return false;
-    ubase = lo > 0 ? a.plan[lo - 1].unit_end : 0;
-    gbase = lo > 0 ? a.plan[lo - 1].group_end : 0;
-    node_base = a.plan[lo].node_base;
-    n = a.plan[lo].n_and_len & 0xff;
-    L = a.plan[lo].n_and_len >> 8;
-    chunk_len = (a.plan[lo].request_and_chunk >> 16) * kKeysPerBlock;
-    return true;
-  }
-  int32_t r;
-  if (!locate_request(gid, true, a, r, ubase, gbase)) return false;
-  node_base = a.node_indptr[r];
-  n = min(max(a.node_indptr[r + 1] - node_base, 0), kMaxTreeNodes);
-  L = max(a.prefix_len[r], 0);
-  chunk_len = chunk_keys(n, a.group, a.rows_per_tile, a.chunk_target, a.chunk_floor);
-  return true;
-}
-
 // Merges the chunk partials of every split (request, kv-head, row tile):
 // with w_c = l_c 2^((m_c - m) c), out = sum_c w_c o_c / sum_c w_c, o_c being
-// chunk c's own normalised output.  One workgroup per 16 rows of a group;
-// each thread owns D/16 columns of one row.
+// chunk c's own normalised output.  One workgroup per 16 rows of one
+// kv-head; each thread owns D/16 columns of one row.  With a plan table the
+// grid holds the split requests' rows only (group_end counts 16-row merge
+// blocks); without one, workgroup b takes rows (b % 8) * 16 .. +15 of
+// (kv-head, row tile) group b / 8 in the scan order, and the workgroups of
+// unsplit requests or past a tile's rows return at once.
 template <int D>
 __global__ __launch_bounds__(kThreads) void tree_attn_combine_kernel(TreeAttnArgs a) {
   constexpr int kRowsPerWg = 16;
   constexpr int TPR = kThreads / kRowsPerWg;  // threads per row
   constexpr int CPT = D / TPR;                // columns per thread (8 or 4)
-  const int64_t gid = blockIdx.x / (kMaxRowsPerTile / kRowsPerWg);
-  const int rblk = blockIdx.x % (kMaxRowsPerTile / kRowsPerWg);
-  if (gid >= a.row_groups) return;
-  int32_t node_base, n, L, chunk_len;
-  int64_t ubase, gbase;
-  if (!group_request(a, gid, node_base, n, L, chunk_len, ubase, gbase)) return;
+  if ((int64_t)blockIdx.x >= a.merge_blocks) return;
+  int32_t node_base, n, L, chunk_len, tile, g, rl;
+  int64_t ubase;
+  const int G = a.group, RT = a.rows_per_tile;
+  if (a.plan_count > 0) {
+    const int lo = __builtin_amdgcn_readfirstlane(find_plan_entry(a, blockIdx.x, true));
+    if (lo < 0) return;
+    const int64_t mbase = lo > 0 ? a.plan[lo - 1].group_end : 0;
+    ubase = lo > 0 ? a.plan[lo - 1].unit_end : 0;
+    node_base = a.plan[lo].node_base;
+    n = a.plan[lo].n_and_len & 0xff;
+    L = a.plan[lo].n_and_len >> 8;
+    chunk_len = (a.plan[lo].request_and_chunk >> 16) * kKeysPerBlock;
+    const int32_t per_head = ceil_div(n * G, kRowsPerWg);
+    if (per_head <= 0) return;
+    const int32_t local = (int32_t)(blockIdx.x - mbase);
+    g = local / per_head;
+    const int32_t row = (local - g * per_head) * kRowsPerWg + (int)threadIdx.x / TPR;
+    if (g >= a.num_kv_heads || row >= n * G) return;
+    tile = row / RT;
+    rl = row - tile * RT;
+  } else {
+    const int64_t gid = blockIdx.x / (kMaxRowsPerTile / kRowsPerWg);
+    const int rblk = blockIdx.x % (kMaxRowsPerTile / kRowsPerWg);
+    if (gid >= a.row_groups) return;
+    int32_t r;
+    int64_t gbase;
+    if (!locate_request(gid, true, a, r, ubase, gbase)) return;
+    node_base = a.node_indptr[r];
+    n = min(max(a.node_indptr[r + 1] - node_base, 0), kMaxTreeNodes);
+    L = max(a.prefix_len[r], 0);
+    chunk_len = chunk_keys(n, G, RT, a.chunk_target, a.chunk_floor);
+    if (n == 0) return;
+    const int32_t tiles_r = row_tiles(n, G, RT);
+    const int64_t u = gid - gbase;
+    tile = (int32_t)(u % tiles_r);
+    g = (int32_t)(u / tiles_r);
+    rl = rblk * kRowsPerWg + (int)threadIdx.x / TPR;
+    if (rl >= min(RT, n * G - tile * RT)) return;
+  }
   if (n == 0 || node_base < 0 || node_base + n > a.total_nodes) return;
   if (chunk_len <= 0 || chunk_len > kMaxChunk || chunk_len % kKeysPerBlock != 0) return;
-  const int G = a.group, RT = a.rows_per_tile;
   const int32_t tiles = row_tiles(n, G, RT);
   const int32_t chunks = prefix_chunks(L, chunk_len);
   if (chunks == 1) return;
-  const int64_t u = gid - gbase;
-  const int32_t tile = (int32_t)(u % tiles);
-  const int32_t g = (int32_t)(u / tiles);
-  const int rl = rblk * kRowsPerWg + (int)threadIdx.x / TPR;
-  const int rows = min(RT, n * G - tile * RT);
-  if (rl >= rows) return;
   const int col = ((int)threadIdx.x % TPR) * CPT;
   const float c = a.scale_log2;
   float mm = -1e30f, ll = 0.f;
@@ -955,7 +961,7 @@ hipError_t launch_tree_attn_bf16(TreeAttnArgs &a, int head_dim, bool needs_combi
     hipLaunchKernelGGL(tree_attn_bf16_kernel<64>, grid, block, 0, stream, a);
   e = hipGetLastError();
   if (e != hipSuccess || !needs_combine) return e;
-  const dim3 cgrid((unsigned)(a.row_groups * (kMaxRowsPerTile / 16)));
+  const dim3 cgrid((unsigned)a.merge_blocks);
   if (head_dim == 128)
     hipLaunchKernelGGL(tree_attn_combine_kernel<128>, cgrid, block, 0, stream, a);
   else
