@@ -119,6 +119,22 @@ def test_balanced_splits_with_uneven_prefixes(torch_cuda):
     check_argmax_accept(b, amax, alen, tok, nodes)
 
 
+@pytest.mark.parametrize("tree", [1, 40])
+def test_every_loop_boundary_of_the_step_pipeline(torch_cuda, tree):
+    """Prefixes of 1 .. 16 whole 32-key blocks, each also one key short and
+    one key long, so every request runs a different mix of the five-step
+    loop, the single fast steps, the branchy tail steps and the masked
+    steps (and, with 40-node trees, two tree blocks after the prefix)."""
+    lens = sorted({32 * k + d for k in range(1, 17) for d in (-1, 0, 1)})
+    rng = np.random.Generator(np.random.PCG64(83 + tree))
+    parents = [random_tree(rng, tree, 8) for _ in lens]
+    b = make_batch(parents=parents, prefix_lens=lens, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                   dtype="bf16", vocab=1000, seed=83 + tree)
+    _, (out, amax, alen, tok, nodes) = run_device(b)
+    check_attention(b, out)
+    check_argmax_accept(b, amax, alen, tok, nodes)
+
+
 def test_out_of_pool_pages_read_as_zero_pages(torch_cuda):
     """Block-table entries outside [0, num_pages) -- negative or past the pool
     -- act as all-zero pages: the call equals, bit for bit, the same batch
