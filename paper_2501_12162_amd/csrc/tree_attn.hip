@@ -9,9 +9,11 @@
 //  * rows of a unit are (node, q-head-in-group) pairs of one kv-head, so the
 //    G query heads that share a kv-head read each K/V byte once (GQA);
 //  * K/V blocks of 32 keys go straight from HBM to LDS with 16-byte
-//    global_load_lds (no staging registers) into a 4-stage ring: three
-//    blocks are in flight while one is multiplied, one barrier per block,
-//    waits counted by hand (vmcnt) so the ring really overlaps;
+//    global_load_lds (no staging registers) into a 5-stage ring: four
+//    stages are in flight while one is multiplied, one barrier per block,
+//    waits counted by hand (vmcnt) so the ring really overlaps; steps that
+//    fetch whole prefix blocks run branch-free, five to a loop iteration,
+//    so their LDS addresses are constants;
 //  * LDS rows are XOR-swizzled in 16-byte chunks so that both the K
 //    fragment reads (16 keys x 16 B per quarter-wave) and the transposed V
 //    reads (ds_read_b64_tr_b16) hit distinct banks;
@@ -24,9 +26,10 @@
 //  * the tree block (the request's own N_r nodes) is masked by 128-bit
 //    ancestor sets built in LDS from parent[];
 //  * prefixes longer than one chunk are split across workgroups; each writes
-//    its partial (reference max, denominator, numerator) and a second,
-//    fully parallel kernel merges them (the kernel boundary makes the
-//    partials of every XCD visible without per-workgroup cache flushes).
+//    its partial (its own normalised output in bf16, reference max and
+//    denominator in fp32) and a second, fully parallel kernel merges them
+//    (the kernel boundary makes the partials of every XCD visible without
+//    per-workgroup cache flushes).
 #include <mutex>
 #include <type_traits>
 
