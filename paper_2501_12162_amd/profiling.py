@@ -9,8 +9,8 @@ Usage (on the GPU machine, after the runs named in each summary's header):
 the tree-attention and argmax kernels, scales each by the factor that makes
 the bench's calibration copy (a device-to-device copy of exactly 256 MiB,
 launched by bench.py before timing) read and write 256 MiB, and stores the
-result with a hash of the kernel sources; ``bench.py`` reports it only while
-the sources still have that hash.
+result with a hash of the kernel sources (comments excluded); ``bench.py``
+reports it only while the sources still have that hash.
 """
 from __future__ import annotations
 
@@ -19,6 +19,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 import statistics
 import sys
 
@@ -34,6 +35,15 @@ def _block(text: str, start: str, end: str) -> str:
     return text[i:text.index(end, i)]
 
 
+def _code_only(text: str) -> str:
+    """The text without its comments and with whitespace runs collapsed, so
+    that edits to comments alone keep the hash (the sources hashed here hold
+    no "//" or "/*" inside string literals)."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_source_hash() -> str:
     """sha256 over the sources that decide the measured kernels' traffic: the
     tree-attention and argmax kernels, their headers, the attention argument
@@ -42,15 +52,16 @@ def kernel_source_hash() -> str:
     h = hashlib.sha256()
     csrc = os.path.join(PKG, "csrc")
     for name in _TRAFFIC_FILES:
-        with open(os.path.join(csrc, name), "rb") as f:
+        with open(os.path.join(csrc, name)) as f:
             h.update(name.encode())
-            h.update(f.read())
+            h.update(_code_only(f.read()).encode())
     with open(os.path.join(csrc, "kernels.h")) as f:
-        h.update(_block(f.read(), "struct TreeAttnArgs", "};").encode())
+        h.update(_code_only(_block(f.read(), "struct TreeAttnArgs", "};")).encode())
     with open(os.path.join(csrc, "adaserve.cpp")) as f:
         text = f.read()
-    h.update(_block(text, "struct AttnShape", "// Beam step:").encode())
-    h.update(_block(text, "int32_t adaserve_tree_attn_verify(", "int32_t adaserve_tree_accept(").encode())
+    h.update(_code_only(_block(text, "struct AttnShape", "// Beam step:")).encode())
+    h.update(_code_only(_block(text, "int32_t adaserve_tree_attn_verify(",
+                                     "int32_t adaserve_tree_accept(")).encode())
     return h.hexdigest()[:16]
 
 
