@@ -18,8 +18,9 @@
 // across the whole chip; the walk -- one workgroup of 1024 threads per
 // request -- then reads them, so an acceptance test costs two logits, a
 // rejection one pass over the node's two rows (the new S), and the bonus
-// draw two passes (segment sums, then a scan of the one segment that holds
-// the target).
+// draw one pass that sums the residual over at most 64 consecutive token
+// ranges ("rounds"), then a second over the one round that holds its
+// target.
 #include <limits.h>
 
 #include "device_common.h"
@@ -33,6 +34,8 @@ constexpr int kThreads = 1024;
 constexpr int kStatsThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kGroupVecs = 4 * kThreads;  // 16-byte vectors per pass iteration (four per thread)
+constexpr int kMaxRounds = 64;            // token ranges whose masses a pass keeps (one per lane)
 
 template <bool BF16>
 __device__ __forceinline__ float elem(const u32x4 &w, int e) {
@@ -55,6 +58,8 @@ struct Shared {
   float red_a[kWaves];
   float red_b[kWaves];
   float scan[kThreads];
+  float rsum[kMaxRounds][kWaves];  // per round and wave: the residual's mass
+  float cum[kMaxRounds];           // inclusive prefix of the rounds' masses, in token order
   int32_t bad;
   int32_t pick;
 };
@@ -82,6 +87,21 @@ struct Residual {
     const float p = __builtin_amdgcn_exp2f((x - mp) * kLog2e) * ip;
     if (!has_q || c == 0.f) return p;
     return fmaxf(p - c * (__builtin_amdgcn_exp2f((y - mq) * kLog2e) * iq), 0.f);
+  }
+};
+
+// Round layout of a pass over a row: its 16-byte vectors go in groups of
+// kGroupVecs (in a group, thread t takes vectors t, t + kThreads, t +
+// 2 kThreads and t + 3 kThreads, so the loads coalesce); gpr consecutive
+// groups form a round, a contiguous token range, at most kMaxRounds of them.
+// The tokens past the last whole vector belong to the last round.
+struct Rounds {
+  int nvec, ngroups, gpr, nrounds;
+  __device__ Rounds(int vocab, int epv) {
+    nvec = vocab / epv;
+    ngroups = max(1, (nvec + kGroupVecs - 1) / kGroupVecs);
+    gpr = (ngroups + kMaxRounds - 1) / kMaxRounds;
+    nrounds = (ngroups + gpr - 1) / gpr;
   }
 };
 
@@ -116,63 +136,136 @@ __device__ float residual_mass(const char *prow, const char *qrow, int vocab, co
   return block_sum(s, sh);
 }
 
+// The residual's mass in each round (per wave in sh.rsum, then the
+// inclusive prefix over the rounds in sh.cum), for the bonus draw; returns
+// the total, the last prefix, so the two always agree.  (A rejection needs
+// only the total: residual_mass above, whose loop measured faster.)
+template <bool BF16>
+__device__ float residual_rounds(const char *prow, const char *qrow, int vocab, const Residual &R, Shared &sh) {
+  constexpr int EPV = BF16 ? 8 : 4;
+  const Rounds rd(vocab, EPV);
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  float acc = 0.f;
+  // round r's mass, summed over the wave, goes to sh.rsum[r][wave]
+  auto flush = [&](int g) {
+    const float ws = wave_sum(acc);
+    if (lane == 0) sh.rsum[g / rd.gpr][wave] = ws;
+    acc = 0.f;
+  };
+  const int nfull = rd.nvec / kGroupVecs;  // groups whose four vectors every thread has
+  for (int g = 0; g < nfull; ++g) {
+    // four vectors of each row in flight per thread
+    const int i0 = g * kGroupVecs + t;
+    u32x4 w[4], z[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      w[k] = *(const u32x4 *)(prow + (int64_t)(i0 + k * kThreads) * 16);
+      z[k] = R.has_q ? *(const u32x4 *)(qrow + (int64_t)(i0 + k * kThreads) * 16) : w[k];
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) acc += R.at(elem<BF16>(w[k], e), elem<BF16>(z[k], e));
+    if ((g + 1) % rd.gpr == 0 && g + 1 < rd.ngroups) flush(g);
+  }
+  // the last, partial group (when there is one) and the tokens past the last vector
+  for (int i = nfull * kGroupVecs + t; i < rd.nvec; i += kThreads) {
+    const u32x4 w = *(const u32x4 *)(prow + (int64_t)i * 16);
+    const u32x4 z = R.has_q ? *(const u32x4 *)(qrow + (int64_t)i * 16) : w;
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) acc += R.at(elem<BF16>(w, e), elem<BF16>(z, e));
+  }
+  for (int v = rd.nvec * EPV + t; v < vocab; v += kThreads)
+    acc += R.at(load_one<BF16>(prow, v), R.has_q ? load_one<BF16>(qrow, v) : 0.f);
+  flush(rd.ngroups - 1);
+  __syncthreads();
+  if (wave == 0) {
+    // lane k: round k's mass, then the inclusive prefix over the rounds
+    float m = 0.f;
+    if (lane < rd.nrounds)
+      for (int w = 0; w < kWaves; ++w) m += sh.rsum[lane][w];
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const float o = __shfl_up(m, off, 64);
+      if (lane >= off) m += o;
+    }
+    if (lane < rd.nrounds) sh.cum[lane] = m;
+  }
+  __syncthreads();
+  return sh.cum[rd.nrounds - 1];
+}
+
 // Inverse-CDF draw from the residual: the smallest v whose cumulative mass
 // (in token order) exceeds u * (total mass); the last token of nonzero mass
-// when rounding leaves the target past the end.  Thread t owns the
-// contiguous segment [t * seg, (t + 1) * seg), seg a multiple of the
-// 16-byte vector, read with vector loads.
+// when rounding leaves the target past the end (-1 when no token has mass).
+// One coalesced pass finds the round that holds the target; that round is
+// then read once more, each thread taking a contiguous run of its vectors so
+// that per-thread sums scan in token order.
 template <bool BF16>
 __device__ int residual_draw(const char *prow, const char *qrow, int vocab, const Residual &R, float u,
                              Shared &sh) {
   constexpr int EPV = BF16 ? 8 : 4;
-  const int t = threadIdx.x;
-  const int seg = ((vocab + kThreads - 1) / kThreads + EPV - 1) / EPV * EPV;
-  const int lo = min(vocab, t * seg), hi = min(vocab, lo + seg);
-  auto seg_pass = [&](float start, float target, bool find, int &found, int &last) {
+  residual_rounds<BF16>(prow, qrow, vocab, R, sh);
+  const Rounds rd(vocab, EPV);
+  const int t = threadIdx.x, lane = t & 63;
+  const float total = sh.cum[rd.nrounds - 1];
+  const float target = u * total;
+  // the first round whose prefix exceeds the target, else the last round
+  // with mass (its last token of nonzero mass is the answer)
+  const bool in = lane < rd.nrounds;
+  const float cl = in ? sh.cum[lane] : 0.f;
+  const float cp = in && lane > 0 ? sh.cum[lane - 1] : 0.f;
+  const uint64_t over = __ballot(in && cl > target);
+  const uint64_t grows = __ballot(in && cl > cp);
+  if (!grows) return -1;
+  const bool find = over != 0;
+  const int rs = find ? __ffsll((unsigned long long)over) - 1 : 63 - __clzll((unsigned long long)grows);
+  const float before = rs > 0 ? sh.cum[rs - 1] : 0.f;
+
+  const int64_t vb = (int64_t)rs * rd.gpr * kGroupVecs;
+  const int64_t ve = min((int64_t)rd.nvec, vb + (int64_t)rd.gpr * kGroupVecs);
+  const int cv = 4 * rd.gpr;  // vectors per thread
+  const int64_t tv0 = min(ve, vb + (int64_t)t * cv), tv1 = min(ve, tv0 + cv);
+  const bool tail = rs == rd.nrounds - 1 && t == kThreads - 1;  // tokens past the last vector
+  // one pass over this thread's tokens, in order: their mass, the last one
+  // with mass, and (find) the first at which start + running mass > goal
+  auto run = [&](float start, float goal, bool stop, int &found, int &last) {
     float acc = start;
     found = -1;
     last = -1;
-    int v = lo;
-    // four vectors of each row in flight per thread
-    for (; v + 4 * EPV <= hi; v += 4 * EPV) {
+    for (int64_t i = tv0; i < tv1; i += 4) {
       u32x4 w[4], z[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        w[k] = *(const u32x4 *)(prow + (int64_t)(v + k * EPV) * (BF16 ? 2 : 4));
-        z[k] = R.has_q ? *(const u32x4 *)(qrow + (int64_t)(v + k * EPV) * (BF16 ? 2 : 4)) : w[k];
+        const int64_t j = min(i + k, tv1 - 1);
+        w[k] = *(const u32x4 *)(prow + j * 16);
+        z[k] = R.has_q ? *(const u32x4 *)(qrow + j * 16) : w[k];
       }
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
+      for (int k = 0; k < 4; ++k) {
+        if (i + k >= tv1) break;
 #pragma unroll
         for (int e = 0; e < EPV; ++e) {
           const float r = R.at(elem<BF16>(w[k], e), elem<BF16>(z[k], e));
           acc += r;
-          if (r > 0.f) last = v + k * EPV + e;
-          if (find && found < 0 && acc > target) found = v + k * EPV + e;
+          const int v = (int)((i + k) * EPV) + e;
+          if (r > 0.f) last = v;
+          if (stop && found < 0 && acc > goal) found = v;
         }
-    }
-    for (; v + EPV <= hi; v += EPV) {
-      const u32x4 w = *(const u32x4 *)(prow + (int64_t)v * (BF16 ? 2 : 4));
-      const u32x4 z = R.has_q ? *(const u32x4 *)(qrow + (int64_t)v * (BF16 ? 2 : 4)) : w;
-#pragma unroll
-      for (int e = 0; e < EPV; ++e) {
-        const float r = R.at(elem<BF16>(w, e), elem<BF16>(z, e));
-        acc += r;
-        if (r > 0.f) last = v + e;
-        if (find && found < 0 && acc > target) found = v + e;
       }
     }
-    for (; v < hi; ++v) {
-      const float r = R.at(load_one<BF16>(prow, v), R.has_q ? load_one<BF16>(qrow, v) : 0.f);
-      acc += r;
-      if (r > 0.f) last = v;
-      if (find && found < 0 && acc > target) found = v;
-    }
-    return acc;
+    if (tail)
+      for (int v = rd.nvec * EPV; v < vocab; ++v) {
+        const float r = R.at(load_one<BF16>(prow, v), R.has_q ? load_one<BF16>(qrow, v) : 0.f);
+        acc += r;
+        if (r > 0.f) last = v;
+        if (stop && found < 0 && acc > goal) found = v;
+      }
+    return acc - start;
   };
   int found, last;
-  const float s = seg_pass(0.f, 0.f, false, found, last);
-  // inclusive prefix of the segment sums (in token order) and the total
+  const float s = run(0.f, 0.f, false, found, last);
+  // inclusive prefix of the threads' sums within the round
   sh.scan[t] = s;
   if (t == 0) sh.pick = -1;
   __syncthreads();
@@ -182,20 +275,17 @@ __device__ int residual_draw(const char *prow, const char *qrow, int vocab, cons
     sh.scan[t] += add;
     __syncthreads();
   }
-  const float total = sh.scan[kThreads - 1];
-  const float incl = sh.scan[t];
-  const float excl = t > 0 ? sh.scan[t - 1] : 0.f;  // exactly the previous segment's end
-  const float target = u * total;
-  // the one segment whose running sum first exceeds the target
-  if (s > 0.f && excl <= target && target < incl) {
+  const float lo = before + (t > 0 ? sh.scan[t - 1] : 0.f);  // exactly the previous thread's end
+  const float hi = before + sh.scan[t];
+  if (find && s > 0.f && lo <= target && target < hi) {
     int f, l2;
-    seg_pass(excl, target, true, f, l2);
+    run(lo, target, true, f, l2);
     sh.pick = f >= 0 ? min(f, last) : last;
   }
   __syncthreads();
   int pick = sh.pick;
   if (pick < 0) {
-    // target at or past the total: the last token of nonzero mass
+    // the round's last token of nonzero mass
     int lastv = last;
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) lastv = max(lastv, __shfl_xor(lastv, off, 64));

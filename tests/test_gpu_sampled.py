@@ -10,11 +10,13 @@ fp64.
   fp32 error of a softmax over 128K logits) must take exactly the oracle's
   path with exactly its tokens.
 * The bonus token: it must be the oracle's, or lie within CDF_TOL of the
-  bonus uniform in the oracle's cumulative distribution (fp32 cumulative sums
-  over at most 128K terms in segments of 128, then a 10-level scan, err by
-  at most ~(128 + 10) * 6e-8 < 1e-5 of the total mass; a diffuse residual
-  has many tokens narrower than that, so such near-boundary draws are
-  expected).
+  bonus uniform in the oracle's cumulative distribution (the kernel's fp32
+  cumulative mass is a 6-level prefix over at most 64 token ranges, each a
+  sum of 16 wave sums; then, inside the range that holds the target, a
+  10-level scan over 1024 threads' sequential sums of at most a few hundred
+  terms: a few hundred roundings of ~6e-8 at most, < 1e-5 of the total mass;
+  a diffuse residual has many tokens narrower than that, so such
+  near-boundary draws are expected).
 * Requests with a near-tie acceptance test are checked for validity only.
 """
 import numpy as np
