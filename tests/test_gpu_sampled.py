@@ -142,6 +142,18 @@ def test_random_batches(torch_cuda, seed, dtype, vocab, noise):
     assert exact >= 10
 
 
+@pytest.mark.parametrize("seed,dtype,vocab", [(5, "f32", 1_100_003), (6, "bf16", 2_200_007)])
+def test_vocabularies_past_64_vector_groups(torch_cuda, seed, dtype, vocab):
+    """Vocabularies whose rows hold more than 64 groups of 4096 vectors, so a
+    bonus draw's token ranges span two groups each and the last one ends in a
+    partial group and a few tokens past the last whole vector."""
+    rng = np.random.Generator(np.random.PCG64(500 + seed))
+    pad = (-vocab) % (8 if dtype == "bf16" else 4)
+    args = _batch(rng, 4, vocab, dtype, 4, 3, 0.5, row_pad=pad)
+    exact = check(torch_cuda, *args[:5], vocab, *args[5:], 8, dtype)
+    assert exact >= 3
+
+
 def test_llama3_8b_batch(torch_cuda):
     """The Llama-3-8B-shaped verification batch: its trees, logits (vocab
     128256, bf16) and draft tokens; draft logits a noisy copy of the target's."""
