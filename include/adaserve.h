@@ -103,7 +103,9 @@ size_t adaserve_tree_attn_workspace_bytes(int32_t num_requests, const int32_t *n
  *   node_indptr       [num_requests + 1] int32 (device), node_indptr_host its copy
  * Supported: dtype F32 or BF16; head_dim 64 or 128; page_size 16; any
  * Hq % Hkv == 0 with Hq / Hkv <= 16; L_r >= 0 (L_r = 0: attention over the
- * root path only).  BF16 computes Q.K^T and P.V on bf16 matrix cores with
+ * root path only); sm_scale finite, and > 0 for BF16
+ * (ADASERVE_ERR_UNSUPPORTED otherwise; F32 takes any finite scale).
+ * BF16 computes Q.K^T and P.V on bf16 matrix cores with
  * fp32 accumulation and rounds the output to bf16 (nearest even); when a
  * prefix is split into chunks, each chunk's own normalised output is kept in
  * bf16 and the chunks are merged with fp32 weights.  F32 computes in fp32

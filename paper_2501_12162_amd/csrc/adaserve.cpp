@@ -413,6 +413,10 @@ int32_t adaserve_tree_attn_verify(int32_t num_requests, const int32_t *node_indp
   int32_t st = validate_attn_shape(num_requests, node_indptr_host, prefix_len_host, num_q_heads, num_kv_heads,
                                    head_dim, page_size, dtype, block_table_stride, shape);
   if (st != ADASERVE_OK) return st;
+  // the bf16 kernel's online softmax takes the running maximum of the scaled
+  // scores in raw units, which orders them only for a positive scale
+  if (dtype == ADASERVE_BF16 && !(sm_scale > 0.f))
+    return fail(ADASERVE_ERR_UNSUPPORTED, "sm_scale %g: the BF16 path needs sm_scale > 0", (double)sm_scale);
   if (num_requests == 0) return ADASERVE_OK;
   if (!node_indptr || !parent || !q || !k_tree || !v_tree || !out || !prefix_len)
     return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");

@@ -24,9 +24,13 @@ Conventions shared by everything that consumes a ``VerifyBatch``:
   ``L_r`` in a request's last page and every page no request owns are
   filled with NaN, so a consumer that reads them shows it.
 * Logits carry a *planted* maximum: every row is drawn from a clipped
-  normal and one position per row (``planted_argmax``) is then set to a
-  value strictly above the clip.  Draft tokens are drawn from the planted
-  positions, so no argmax is ever computed here.
+  normal and one position per row is then set to a value strictly above
+  the clip; in a share ``tie_rate`` of the rows the same value is planted
+  at two (sometimes three) distinct positions, the rate at which natural
+  bf16 rows of a large vocabulary tie at their maximum.  ``planted_argmax``
+  is the lowest planted position (an integer minimum over the positions
+  drawn here) and draft tokens are drawn from it, so no argmax is ever
+  computed here.
 """
 from __future__ import annotations
 
@@ -135,8 +139,9 @@ class VerifyBatch:
     k_pages: np.ndarray             # [P, Hkv, ps, D]
     v_pages: np.ndarray             # [P, Hkv, ps, D]
     logits: np.ndarray              # [T, row_stride]  (uint16 bf16 bits or float32)
-    planted_argmax: np.ndarray      # int32 [T]
+    planted_argmax: np.ndarray      # int32 [T]  lowest planted maximum position
     draft_tokens: np.ndarray        # int32 [T]
+    planted_ties: Optional[np.ndarray] = None   # int32 [T]  planted maximum positions per row
     meta: dict = field(default_factory=dict)
 
     @property
@@ -206,6 +211,7 @@ def make_batch(
     name: str = "custom",
     rng: Optional[np.random.Generator] = None,
     reserve_tokens: int = 0,
+    tie_rate: float = 0.0,
 ) -> VerifyBatch:
     """Draw every tensor of one verify batch for the given tree shapes.
 
@@ -214,6 +220,8 @@ def make_batch(
     extends every request's block table to cover that many positions past its
     prefix (pages for the accepted path to be committed to; NaN-filled like
     every slot past the prefix).  With the default 0 nothing changes.
+    ``tie_rate`` is the share of logit rows whose maximum is planted at two
+    (one in 30 of them: three) distinct positions instead of one.
     """
     if dtype not in ("bf16", "f32"):
         raise ValueError("dtype must be 'bf16' or 'f32'")
@@ -266,11 +274,23 @@ def make_batch(
     k_pages[~owned] = nan
     v_pages[~owned] = nan
 
-    # Logits with a planted unique maximum per row (drawn a block of rows
-    # at a time).
+    # Logits with a planted maximum per row (drawn a block of rows at a
+    # time); tied rows get the same value at one or two more positions.
     row_stride = vocab + row_pad
     planted = (rng.integers(0, vocab, size=T, dtype=np.int64).astype(np.int32)
                if vocab else np.zeros(T, np.int32))
+    ties = np.ones(T, dtype=np.int32)
+    extra = {}
+    if tie_rate > 0 and vocab >= 3:
+        tied = np.nonzero(rng.random(T) < tie_rate)[0]
+        for i in tied:
+            k = 3 if rng.random() < 1.0 / 30 else 2
+            pos = {int(planted[i])}
+            while len(pos) < k:
+                pos.add(int(rng.integers(0, vocab)))
+            extra[int(i)] = sorted(pos)
+            ties[i] = k
+            planted[i] = min(pos)
     logits = np.empty((T, row_stride), dtype=np.uint16 if dtype == "bf16" else np.float32)
     clip = np.float32(7.5 * logit_std)
     rows_per = max(1, _CHUNK // max(row_stride, 1))
@@ -281,6 +301,9 @@ def make_batch(
         np.clip(body, -clip, clip, out=body)
         if vocab:
             body[np.arange(b - a), planted[a:b]] = np.float32(8.0 * logit_std)
+            for i in range(a, b):
+                for pos in extra.get(i, ()):
+                    body[i - a, pos] = np.float32(8.0 * logit_std)
         if dtype == "bf16":
             f32_to_bf16_bits(body, out=logits[a:b])
         else:
@@ -303,7 +326,7 @@ def make_batch(
         page_size=ps, sm_scale=1.0 / math.sqrt(D), vocab=vocab, p_match=p_match,
         node_indptr=indptr, parent=parent, prefix_len=L, block_table=block_table,
         q=q, k_tree=k_tree, v_tree=v_tree, k_pages=k_pages, v_pages=v_pages,
-        logits=logits, planted_argmax=planted, draft_tokens=draft,
+        logits=logits, planted_argmax=planted, draft_tokens=draft, planted_ties=ties,
         meta={"seed": seed},
     )
 
@@ -319,6 +342,12 @@ WORKLOAD_NAMES = {
     4: "llama3-70b-shape-bf16 (32 req, 64/8 heads, D=128, L~U[2048,8192], 32-96 nodes depth<=10, p=0.6)",
     5: "long-context-bf16 (8 req, 32/8 heads, D=128, L=32768, 32 nodes: even chains, odd random, p=0.8)",
 }
+
+# Share of bf16 N(0, 2) logit rows over a 128256-token vocabulary whose
+# maximum value occurs more than once (about 6-8.5% in samples of a few
+# hundred rows, almost always twice); the bf16 workloads plant ties at this
+# rate.
+NATURAL_TIE_RATE = 0.085
 
 SHORT_NAMES = {1: "tiny_f32", 2: "llama3_8b", 3: "mixed_slo", 4: "llama3_70b_shape", 5: "long_context"}
 
@@ -369,6 +398,8 @@ def make_config(n: int, seed: Optional[int] = None) -> VerifyBatch:
                   p_match=0.8, logit_std=2.0)
     else:
         raise ValueError("workloads are numbered 1..5")
+    if kw["dtype"] == "bf16":
+        kw["tie_rate"] = NATURAL_TIE_RATE
     b = make_batch(parents=parents, prefix_lens=lens, page_size=16, seed=seed,
                    name=SHORT_NAMES[n], rng=rng, **kw)
     b.meta["workload"] = WORKLOAD_NAMES[n]

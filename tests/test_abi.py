@@ -94,6 +94,8 @@ def _verify(lib, **kw):
     (dict(num_pages=-1), ada.ADASERVE_ERR_INVALID_ARGUMENT),
     (dict(num_pages=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
     (dict(scale=float("nan")), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(scale=0.0), ada.ADASERVE_ERR_UNSUPPORTED),
+    (dict(scale=-0.125), ada.ADASERVE_ERR_UNSUPPORTED),
     (dict(q=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
     (dict(out=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
     (dict(parent=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),

@@ -62,22 +62,17 @@ def check_argmax_accept(b, amax, alen, tok, nodes, max_accept=128):
     np.testing.assert_array_equal(nodes, rn)
 
 
-def sample_nodes(b):
-    ip = b.node_indptr
-    s = set()
-    for r in range(b.num_requests):
-        a, e = int(ip[r]), int(ip[r + 1])
-        s.update({a, e - 1, (a + e) // 2})
-    return sorted(s)
-
-
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
 def test_named_workload(torch_cuda, cfg):
+    """Every node and every head of the named workload against the oracle;
+    the bf16 workloads' logits tie at the maximum in some rows."""
     b = cached_config(cfg)
     print("workload", cfg, b.name, "T", b.total_nodes, flush=True)
     _, (out, amax, alen, tok, nodes) = run_device(b)
-    check_attention(b, out, None if cfg == 1 else sample_nodes(b))
+    check_attention(b, out)
     check_argmax_accept(b, amax, alen, tok, nodes)
+    if b.dtype == "bf16":
+        assert (b.planted_ties > 1).sum() >= 0.04 * b.total_nodes
 
 
 def _ragged_batch(dtype, head_dim, seed, hq=8, hkv=2):
@@ -92,8 +87,10 @@ def _ragged_batch(dtype, head_dim, seed, hq=8, hkv=2):
 
 
 @pytest.mark.parametrize("dtype,head_dim,hq,hkv", [("bf16", 128, 8, 2), ("bf16", 64, 16, 2),
-                                                   ("bf16", 128, 16, 16), ("f32", 128, 4, 2),
-                                                   ("f32", 64, 8, 8)])
+                                                   ("bf16", 128, 16, 16), ("bf16", 128, 4, 2),
+                                                   ("bf16", 128, 32, 2), ("bf16", 64, 16, 1),
+                                                   ("f32", 128, 4, 2), ("f32", 64, 8, 8),
+                                                   ("f32", 64, 32, 2)])
 def test_ragged_tiles_chunks_and_tails(torch_cuda, dtype, head_dim, hq, hkv):
     b = _ragged_batch(dtype, head_dim, seed=31 + head_dim + hq, hq=hq, hkv=hkv)
     d, (out, amax, alen, tok, nodes) = run_device(b)
@@ -115,7 +112,7 @@ def test_balanced_splits_with_uneven_prefixes(torch_cuda):
                    dtype="bf16", vocab=1000, seed=57)
     d, (out, amax, alen, tok, nodes) = run_device(b)
     assert d.workspace_bytes > 0
-    check_attention(b, out, sample_nodes(b))
+    check_attention(b, out)
     check_argmax_accept(b, amax, alen, tok, nodes)
 
 
@@ -168,7 +165,7 @@ def test_out_of_pool_pages_read_as_zero_pages(torch_cuda):
     assert d.workspace_bytes > 0
     _, (out_zero, *_) = run_device(b_zero)
     np.testing.assert_array_equal(out_bad, out_zero)
-    check_attention(b_zero, out_zero, sample_nodes(b_zero))
+    check_attention(b_zero, out_zero)
 
 
 def test_verification_step_replayed_from_a_graph(torch_cuda):
@@ -207,7 +204,7 @@ def test_verification_step_replayed_from_a_graph(torch_cuda):
         d.step()   # eager work between replays
         torch.cuda.synchronize()
     out, amax, alen, tok, nodes = d.results()
-    check_attention(b, out, sample_nodes(b))
+    check_attention(b, out)
     check_argmax_accept(b, amax, alen, tok, nodes, max_accept=16)
 
 
@@ -334,14 +331,19 @@ def test_native_library_is_the_in_tree_build(torch_cuda):
 
 
 def test_many_requests_use_the_scan_path(torch_cuda):
-    # more requests than the kernel-argument plan holds: units are found by
-    # scanning node_indptr / prefix_len on the device
+    """More requests than the kernel-argument plan holds: attention units and
+    split-KV merge blocks are found by scanning node_indptr / prefix_len on
+    the device.  A quarter of the requests have prefixes of 2000-6000 keys,
+    which the planner splits, so the merge kernel's scan branch runs too."""
     rng = np.random.Generator(np.random.PCG64(77))
     parents = [random_tree(rng, int(rng.integers(1, 12))) for _ in range(260)]
     lens = [int(x) for x in rng.integers(0, 300, size=260)]
+    for r in range(0, 260, 4):
+        lens[r] = int(rng.integers(2000, 6001))
     b = make_batch(parents=parents, prefix_lens=lens, num_q_heads=8, num_kv_heads=2, head_dim=128,
                    dtype="bf16", vocab=256, seed=77)
-    _, (out, amax, alen, tok, nodes) = run_device(b)
+    d, (out, amax, alen, tok, nodes) = run_device(b)
+    assert d.workspace_bytes > 0
     check_attention(b, out)
     check_argmax_accept(b, amax, alen, tok, nodes)
 

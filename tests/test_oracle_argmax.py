@@ -67,6 +67,15 @@ def test_planted_maxima_of_named_workloads(n):
     rows = np.arange(0, b.total_nodes, 7)
     got = oracle.node_argmax(b.logits, b.vocab, b.dtype, rows=rows)
     np.testing.assert_array_equal(got, b.planted_argmax[rows])
+    if b.dtype == "bf16":
+        # ties at about the natural bf16 rate, resolved to the lowest index;
+        # every row of a tie is checked
+        tied = np.nonzero(b.planted_ties > 1)[0]
+        assert 0.04 * b.total_nodes <= tied.size <= 0.14 * b.total_nodes, tied.size
+        np.testing.assert_array_equal(oracle.node_argmax(b.logits, b.vocab, b.dtype, rows=tied),
+                                      b.planted_argmax[tied])
+        x = bf16_bits_to_f32(b.logits[tied, :b.vocab])
+        assert ((x == x.max(axis=1, keepdims=True)).sum(axis=1) == b.planted_ties[tied]).all()
 
 
 def test_single_column_and_empty():
