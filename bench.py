@@ -5,8 +5,12 @@ one MI355X, with the dominant kernel's roofline and the CPU oracle's rate.
 A step is one full verification pass over one batch: paged tree attention
 (+ split-KV combine), per-node argmax over the vocabulary, acceptance.
 Inputs are seeded synthetic tensors shaped like the workload named by
-``--workload`` (default: the Llama-3-8B-shaped batch), resident in device
-memory before timing starts.  Consecutive steps cycle through several
+``--workload`` (default: the long-context batch, 8 requests over 32768-token
+prefixes, the bandwidth-bound headline), resident in device memory before
+timing starts.  The three steps run one after another on one stream;
+``--overlap`` runs the per-node argmax (which reads only the logits) on a
+second stream of the same priority beside the attention, joined before the
+acceptance.  Consecutive steps cycle through several
 copies of the inputs so that no step finds its K/V or logits in the 256 MB
 last-level (MALL) cache left behind by the previous one.
 
@@ -34,8 +38,13 @@ def parse_args():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=10)
-    p.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5],
-                   help="1 tiny-f32, 2 llama3-8b (default), 3 mixed-slo, 4 70b-shape, 5 long-context")
+    p.add_argument("--workload", type=int, default=5, choices=[1, 2, 3, 4, 5],
+                   help="1 tiny-f32, 2 llama3-8b, 3 mixed-slo, 4 70b-shape, 5 long-context (default)")
+    p.add_argument("--overlap", action="store_true",
+                   help="run argmax on a second stream beside attention instead of after it")
+    p.add_argument("--mfma-workload", type=int, default=4, choices=[0, 1, 2, 3, 4, 5],
+                   help="also time tree attention alone on this (matrix-core bound) workload and "
+                        "report its MFMA fraction; 0 = skip")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="approximate CPU time budget of the oracle baseline sample")
@@ -122,52 +131,98 @@ def make_replicas(dev, count):
     return reps
 
 
-def cpu_baseline(b, budget_s):
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_pass(b, nodes=None):
+    """One oracle pass (attention of `nodes` (all: None) over every q-head,
+    argmax of their rows, acceptance of the whole batch); per-stage seconds."""
+    import oracle
+    t0 = time.perf_counter()
+    oracle.tree_attn_batch(b, nodes=nodes)
+    t1 = time.perf_counter()
+    amax = oracle.node_argmax(b.logits, b.vocab, b.dtype, rows=nodes)
+    t2 = time.perf_counter()
+    if nodes is not None:
+        amax = b.planted_argmax   # the rows not scanned: acceptance needs every node's choice
+    oracle.tree_accept(b.node_indptr, b.parent, b.draft_tokens, amax, 128)
+    t3 = time.perf_counter()
+    return t1 - t0, t2 - t1, t3 - t2
+
+
+def cpu_baseline(b, budget_s, one_thread=True):
     """The oracle (untuned) on a bounded sample of the same workload.
 
     When one full pass (attention of every node, argmax of every row,
     acceptance of every request) fits the budget, full passes are repeated
-    until the budget is used; otherwise an even spread of nodes is timed.
+    until the budget is used; otherwise an even spread of nodes (attention
+    and argmax of their rows) is timed with the acceptance of the whole
+    batch, and the rate is scaled to the whole batch.  Per-stage seconds are
+    per full pass.  With `one_thread`, the same oracle on one thread times
+    the tiny workload (whole batch) and an even spread of 64 nodes of the
+    Llama-3-8B-shaped workload.
     """
     import numpy as np
     import oracle
     threads = oracle.num_threads()
     T = b.total_nodes
     probe = np.unique(np.linspace(0, T - 1, min(T, 8)).round().astype(np.int64))
-    t0 = time.perf_counter()
-    oracle.tree_attn_batch(b, nodes=probe)
-    oracle.node_argmax(b.logits, b.vocab, b.dtype, rows=probe)
-    per_node = max((time.perf_counter() - t0) / probe.size, 1e-6)
+    ta, tm, _ = _oracle_pass(b, probe)
+    per_node = max((ta + tm) / probe.size, 1e-6)
     if per_node * T <= budget_s:
-        passes, nodes_done, t_total = 0, 0, 0.0
-        while t_total < budget_s or passes == 0:
-            t0 = time.perf_counter()
-            oracle.tree_attn_batch(b)
-            amax = oracle.node_argmax(b.logits, b.vocab, b.dtype)
-            oracle.tree_accept(b.node_indptr, b.parent, b.draft_tokens, amax, 128)
-            t_total += time.perf_counter() - t0
-            passes += 1
-            nodes_done += T
-        value = nodes_done / t_total
+        passes, sa, sm, sc = 0, 0.0, 0.0, 0.0
+        while sa + sm + sc < budget_s or passes == 0:
+            ta, tm, tc = _oracle_pass(b)
+            sa, sm, sc, passes = sa + ta, sm + tm, sc + tc, passes + 1
+        t_total = sa + sm + sc
+        value = T * passes / t_total
+        stages = {"attention": sa / passes, "argmax": sm / passes, "accept": sc / passes}
         sample = ("the whole batch (attention of all %d nodes over all q-heads, vocab argmax of "
                   "every row, acceptance of every request), %d full passes, fp64, %.1f s wall"
                   % (T, passes, t_total))
     else:
         want = int(min(T, max(1, budget_s / per_node)))
         sel = np.unique(np.linspace(0, T - 1, want).round().astype(np.int64))
-        t0 = time.perf_counter()
-        oracle.tree_attn_batch(b, nodes=sel)
-        oracle.node_argmax(b.logits, b.vocab, b.dtype, rows=sel)
-        t_part = time.perf_counter() - t0
-        t0 = time.perf_counter()
-        oracle.tree_accept(b.node_indptr, b.parent, b.draft_tokens, b.planted_argmax, 128)
-        t_accept = time.perf_counter() - t0
-        value = 1.0 / (t_part / sel.size + t_accept / T)
+        ta, tm, tc = _oracle_pass(b, sel)
+        value = 1.0 / ((ta + tm) / sel.size + tc / T)
+        stages = {"attention": ta * T / sel.size, "argmax": tm * T / sel.size, "accept": tc}
         sample = ("%d of %d tree nodes (attention over all q-heads + vocab argmax of their rows, "
                   "evenly spread over the batch) plus acceptance of the whole batch; fp64; "
-                  "%.1f s wall" % (sel.size, T, t_part + t_accept))
-    return {"value": value, "unit": "tree tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": sample}
+                  "%.1f s wall; stage times scaled to the whole batch" % (sel.size, T, ta + tm + tc))
+    res = {"value": value, "unit": "tree tokens/s", "cores": int(threads), "kind": "oracle",
+           "sample": sample, "cpu_model": cpu_model(),
+           "stage_s_per_pass": stages}
+    if one_thread:
+        from paper_2501_12162_amd.workload import WORKLOAD_NAMES, make_config
+        one = {}
+        oracle.set_num_threads(1)
+        try:
+            for n in (1, 2):
+                bn = b if b.meta.get("config") == n else make_config(n)
+                Tn = bn.total_nodes
+                sel = None if n == 1 else np.unique(np.linspace(0, Tn - 1, 64).round().astype(np.int64))
+                reps, ta, tm, tc = 0, 0.0, 0.0, 0.0
+                while reps == 0 or (n == 1 and ta + tm + tc < 0.5):
+                    a_, m_, c_ = _oracle_pass(bn, sel)
+                    ta, tm, tc, reps = ta + a_, tm + m_, tc + c_, reps + 1
+                k = Tn if sel is None else sel.size
+                rate = 1.0 / ((ta + tm) / (k * reps) + tc / (Tn * reps))
+                one[WORKLOAD_NAMES[n].split(" ")[0]] = {
+                    "value": rate, "unit": "tree tokens/s",
+                    "sample": ("whole batch, %d passes" % reps) if sel is None
+                    else "%d of %d nodes evenly spread + acceptance of the whole batch" % (k, Tn)}
+        finally:
+            oracle.set_num_threads(threads)
+        res["one_thread"] = one
+    return res
 
 
 def measured_traffic(workload: int, kernel: str):
@@ -191,6 +246,40 @@ def measured_traffic(workload: int, kernel: str):
     return total
 
 
+def attention_alone(n, calls=10):
+    """Tree attention alone, back to back, on workload `n` (its K/V exceed the
+    MALL, so no call finds the previous one's data there): mean event-timed
+    duration per call and its roofline fractions."""
+    import numpy as np
+    import torch
+    from paper_2501_12162_amd.device import DeviceBatch
+    from paper_2501_12162_amd.workload import WORKLOAD_NAMES, make_config
+    b = make_config(n)
+    costs = algorithmic_costs(b)
+    d = DeviceBatch(b)
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        d.attention(stream)
+    torch.cuda.synchronize()
+    ev = [KernelTimer() for _ in range(calls + 1)]
+    ev[0].record(stream)
+    for i in range(calls):
+        d.attention(stream)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    us = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(calls)]) * 1e3
+    mean = float(us.mean())
+    return {"workload": WORKLOAD_NAMES[n], "tree_attn_us": mean, "tree_attn_p50_us": float(np.median(us)),
+            "mfma_frac": costs["attn_flops"] / (mean * 1e-6) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
+            "hbm_frac": costs["attn_bytes"] / (mean * 1e-6) / 1e9 / HBM_PEAK_GBS,
+            "alg_flops": costs["attn_flops"], "alg_bytes": costs["attn_bytes"],
+            "traffic": measured_traffic(n, "tree_attn"), "calls": calls}
+
+
+def progress(msg):
+    print("bench: " + msg, file=sys.stderr, flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -211,6 +300,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev_name = torch.cuda.get_device_name(0)
 
+    progress("drawing workload %d" % args.workload)
     b = make_config(args.workload)
     costs = algorithmic_costs(b)
     dev = DeviceBatch(b)
@@ -219,9 +309,19 @@ def main():
     n_rep = max(2, math.ceil(3 * MALL_BYTES / step_bytes) + 1)
     reps = make_replicas(dev, n_rep)
     stream = torch.cuda.current_stream()
+    # argmax beside attention: a second stream of the default priority, forked
+    # after the previous step's acceptance (which reads the argmax output)
+    # and joined before this step's acceptance
+    side = torch.cuda.Stream() if args.overlap else None
+    fork, join = torch.cuda.Event(), torch.cuda.Event()
 
     def run_step(i, ev=None):
+        """One pass; `ev` = six timers around attention, argmax, acceptance."""
         rp = reps[i % n_rep]
+        am = stream if side is None else side
+        if side is not None:
+            fork.record(stream)
+            side.wait_event(fork)
         if ev is not None:
             ev[0].record(stream)
         ada.adaserve_tree_attn_verify(
@@ -229,24 +329,32 @@ def main():
             q=rp["q"], k_tree=rp["k_tree"], v_tree=rp["v_tree"], k_pages=rp["k_pages"],
             v_pages=rp["v_pages"], block_table=dev.block_table, prefix_len=dev.prefix_len,
             prefix_len_host=dev.prefix_len_host, sm_scale=b.sm_scale, out=dev.out,
-            workspace=dev.workspace)
+            workspace=dev.workspace, stream=stream)
         if ev is not None:
             ev[1].record(stream)
-        ada.adaserve_node_argmax(rp["logits"], b.vocab, dev.target_argmax)
+            ev[2].record(am)
+        ada.adaserve_node_argmax(rp["logits"], b.vocab, dev.target_argmax, stream=am)
         if ev is not None:
-            ev[2].record(stream)
+            ev[3].record(am)
+        if side is not None:
+            join.record(side)
+            stream.wait_event(join)
+        if ev is not None:
+            ev[4].record(stream)
         ada.adaserve_tree_accept(node_indptr=dev.node_indptr, parent=dev.parent,
                                  draft_tokens=dev.draft_tokens, target_argmax=dev.target_argmax,
                                  max_accept=dev.max_accept, accept_len=dev.accept_len,
-                                 accept_tokens=dev.accept_tokens, accept_nodes=dev.accept_nodes)
+                                 accept_tokens=dev.accept_tokens, accept_nodes=dev.accept_nodes,
+                                 stream=stream)
         if ev is not None:
-            ev[3].record(stream)
+            ev[5].record(stream)
 
     # calibration copy of a known size (reference for HBM byte counters)
     calib_src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda").fill_(1)
     calib_dst = torch.empty_like(calib_src)
     calib_dst.copy_(calib_src)
 
+    progress("timing %d steps after %d warm-up steps" % (args.steps, args.warmup))
     for i in range(args.warmup):
         run_step(i)
     torch.cuda.synchronize()
@@ -261,7 +369,7 @@ def main():
     # with the rocprofv3 kernel trace.
     n_inst = max(1, args.steps // EVENT_EVERY)
     sampled_steps = list(range(args.steps - n_inst, args.steps))
-    events = {i: [KernelTimer() for _ in range(4)] for i in sampled_steps}
+    events = {i: [KernelTimer() for _ in range(6)] for i in sampled_steps}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -390,8 +498,9 @@ def main():
     sampled_len = s_len.cpu().numpy()
 
     attn_ms = np.array([e[0].elapsed_time(e[1]) for e in events.values()])
-    argmax_ms = np.array([e[1].elapsed_time(e[2]) for e in events.values()])
-    accept_ms = np.array([e[2].elapsed_time(e[3]) for e in events.values()])
+    argmax_ms = np.array([e[2].elapsed_time(e[3]) for e in events.values()])
+    accept_ms = np.array([e[4].elapsed_time(e[5]) for e in events.values()])
+    step_ms = np.array([e[0].elapsed_time(e[5]) for e in events.values()])
 
     # sanity: the last step's argmax must equal the planted maxima
     got = dev.target_argmax.cpu().numpy()
@@ -400,10 +509,17 @@ def main():
         sys.exit(3)
     alen = dev.accept_len.cpu().numpy()
 
+    extra = None
+    if args.mfma_workload and args.mfma_workload != args.workload:
+        del reps, dev
+        progress("attention alone on workload %d" % args.mfma_workload)
+        extra = attention_alone(args.mfma_workload)
+
     T = b.total_nodes
     ms_per_step = wall * 1e3 / args.steps
     value = T * args.steps / wall
-    attn_us, argmax_us, accept_us = (float(x.mean()) * 1e3 for x in (attn_ms, argmax_ms, accept_ms))
+    attn_us, argmax_us, accept_us, step_us = (float(x.mean()) * 1e3
+                                              for x in (attn_ms, argmax_ms, accept_ms, step_ms))
     attn_gbs = costs["attn_bytes"] / (attn_us * 1e-6) / 1e9
     argmax_gbs = costs["argmax_bytes"] / (argmax_us * 1e-6) / 1e9
     attn_tflops = costs["attn_flops"] / (attn_us * 1e-6) / 1e12
@@ -445,6 +561,7 @@ def main():
             "page_size": b.page_size, "vocab": b.vocab,
             "input_copies": n_rep,
             "instrumented_steps": len(sampled_steps),
+            "argmax_beside_attention": bool(args.overlap),
         },
         "roofline": roof,
         "kernels": {
@@ -454,7 +571,7 @@ def main():
             "node_argmax_us": argmax_us, "node_argmax_hbm_frac": argmax_gbs / HBM_PEAK_GBS,
             "node_argmax_alg_bytes": costs["argmax_bytes"],
             "tree_accept_us": accept_us,
-            "step_event_sum_us": attn_us + argmax_us + accept_us,
+            "step_event_span_us": step_us,
             "kv_commit_us": commit_us,
             "kv_commit_rows": committed_rows,
             "kv_commit_bytes": committed_rows * 4 * b.num_kv_heads * b.head_dim * (2 if is_bf16 else 4),
@@ -466,19 +583,22 @@ def main():
             "beam_step_rows": int(bb.logits.shape[0]),
             "beam_step_hbm_frac": beam_bytes / (beam_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
             "path_hbm_frac": (costs["attn_bytes"] + costs["argmax_bytes"])
-            / ((attn_us + argmax_us + accept_us) * 1e-6) / 1e9 / HBM_PEAK_GBS,
+            / (step_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
             "percentiles_us": {
                 name: {"p10": float(np.percentile(x, 10)) * 1e3, "p50": float(np.median(x)) * 1e3,
                        "p90": float(np.percentile(x, 90)) * 1e3}
                 for name, x in (("tree_attn", attn_ms), ("node_argmax", argmax_ms), ("tree_accept", accept_ms),
-                                ("step", attn_ms + argmax_ms + accept_ms))
+                                ("step", step_ms))
             },
         },
         "accepted_tokens_per_step": int(alen.sum()),
         "accepted_tokens_per_s": float(alen.sum()) * args.steps / wall,
         "device": dev_name,
     }
+    if extra is not None:
+        line["mfma_bound_attention"] = extra
     if not args.no_cpu_baseline:
+        progress("oracle baseline on the host cores")
         line["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds)
     print(json.dumps(line), flush=True)
 

@@ -46,9 +46,12 @@ def _load():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_LIB_PATH):
-        build()
-    lib = ctypes.CDLL(_LIB_PATH)
+    path = os.environ.get("ADASERVE_ORACLE_LIB")   # an instrumented build (CPU sanitizer run)
+    if not path:
+        path = _LIB_PATH
+        if not os.path.exists(path):
+            build()
+    lib = ctypes.CDLL(path)
     P = ctypes.c_void_p
     i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
     lib.oracle_tree_attn.restype = i32

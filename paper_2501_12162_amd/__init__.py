@@ -61,7 +61,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     global _lib
     if _lib is not None and path is None:
         return _lib
-    p = path or LIB_PATH
+    p = path or library_path()
     if not os.path.exists(p):
         raise ImportError("libadaserve.so is not built (%s); run `python -m paper_2501_12162_amd.build`" % p)
     lib = ctypes.CDLL(p)
@@ -75,7 +75,9 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
 
 
 def library_path() -> str:
-    return LIB_PATH
+    """The in-tree build, or the build named by ADASERVE_LIBRARY (the CPU
+    sanitizer run points it at an instrumented build of the same sources)."""
+    return os.environ.get("ADASERVE_LIBRARY") or LIB_PATH
 
 
 def _check(status: int) -> None:

@@ -4,19 +4,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-namespace adaserve {
+#include "plan.h"
 
-// Requests in descending order of per-unit cost, carried in the kernel
-// arguments so a workgroup finds its unit without touching memory.  Batches
-// with more requests fall back to a scan of node_indptr / prefix_len.
-constexpr int kPlanMax = 160;
-struct PlanEntry {
-  int32_t unit_end;   // exclusive end of this request's units in dispatch order
-  int32_t group_end;  // exclusive end of its 16-row merge blocks, same order (none when unsplit)
-  int32_t request_and_chunk;  // request (bits 0..15) | prefix keys per unit / 32 << 16
-  int32_t node_base;  // node_indptr[request]
-  int32_t n_and_len;  // tree nodes (bits 0..7) | prefix length << 8
-};
+namespace adaserve {
 
 struct TreeAttnArgs {
   const int32_t *node_indptr;  // [B+1]

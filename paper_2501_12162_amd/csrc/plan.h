@@ -69,6 +69,33 @@ ADASERVE_HD int64_t request_units(int32_t n_nodes, int32_t prefix_len, int32_t n
          prefix_chunks(prefix_len, chunk_keys(n_nodes, group, rows_per_tile, chunk_target, floor_mult));
 }
 
+// Requests in descending order of per-unit cost, carried in the kernel
+// arguments so a workgroup finds its unit without touching memory.  Batches
+// with more requests fall back to a scan of node_indptr / prefix_len.
+constexpr int kPlanMax = 160;
+struct PlanEntry {
+  int32_t unit_end;   // exclusive end of this request's units in dispatch order
+  int32_t group_end;  // exclusive end of its 16-row merge blocks, same order (none when unsplit)
+  int32_t request_and_chunk;  // request (bits 0..15) | prefix keys per unit / 32 << 16
+  int32_t node_base;  // node_indptr[request]
+  int32_t n_and_len;  // tree nodes (bits 0..7) | prefix length << 8
+};
+
+// Field packing of a plan entry: request < kPlanMax, blocks per chunk <=
+// kMaxChunk / 32, tree nodes <= kMaxTreeNodes, prefix length < 2^23 (the
+// host validation's limit), so every field fits its bits.
+ADASERVE_HD int32_t pack_request_chunk(int32_t request, int32_t chunk_blocks) {
+  return (int32_t)((uint32_t)request | ((uint32_t)chunk_blocks << 16));
+}
+ADASERVE_HD int32_t plan_request(int32_t v) { return v & 0xffff; }
+ADASERVE_HD int32_t plan_chunk_keys(int32_t v) { return (int32_t)((uint32_t)v >> 16) * kKeysPerBlock; }
+ADASERVE_HD int32_t pack_nodes_len(int32_t n, int32_t len) {
+  return (int32_t)((uint32_t)n | ((uint32_t)len << 8));
+}
+ADASERVE_HD int32_t plan_nodes(int32_t v) { return v & 0xff; }
+ADASERVE_HD int32_t plan_prefix_len(int32_t v) { return (int32_t)((uint32_t)v >> 8); }
+constexpr int32_t kMaxPrefixLen = (1 << 23) - 1;
+
 // Workgroup id -> logical unit id.  Hardware deals consecutive workgroup ids
 // to the XCDs round-robin.  Logical units are grouped in runs of kXcdRun
 // consecutive ids; run k goes to XCD k % kXcds.  Neighbouring units (the row

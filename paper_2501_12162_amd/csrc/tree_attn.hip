@@ -197,12 +197,12 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
     // the dispatch-ordered plan in the kernel arguments
     const int lo = __builtin_amdgcn_readfirstlane(find_plan_entry(a, uid, false));
     if (lo < 0) return;
-    r = a.plan[lo].request_and_chunk & 0xffff;
-    chunk_len = (a.plan[lo].request_and_chunk >> 16) * kKeysPerBlock;
+    r = plan_request(a.plan[lo].request_and_chunk);
+    chunk_len = plan_chunk_keys(a.plan[lo].request_and_chunk);
     ubase = lo > 0 ? a.plan[lo - 1].unit_end : 0;
     node_base = a.plan[lo].node_base;
-    n = a.plan[lo].n_and_len & 0xff;
-    L = a.plan[lo].n_and_len >> 8;
+    n = plan_nodes(a.plan[lo].n_and_len);
+    L = plan_prefix_len(a.plan[lo].n_and_len);
   } else {
     int64_t gbase;
     if (!locate_request(uid, false, a, r, ubase, gbase)) return;
@@ -711,9 +711,9 @@ __global__ __launch_bounds__(kThreads) void tree_attn_combine_kernel(TreeAttnArg
     const int64_t mbase = lo > 0 ? a.plan[lo - 1].group_end : 0;
     ubase = lo > 0 ? a.plan[lo - 1].unit_end : 0;
     node_base = a.plan[lo].node_base;
-    n = a.plan[lo].n_and_len & 0xff;
-    L = a.plan[lo].n_and_len >> 8;
-    chunk_len = (a.plan[lo].request_and_chunk >> 16) * kKeysPerBlock;
+    n = plan_nodes(a.plan[lo].n_and_len);
+    L = plan_prefix_len(a.plan[lo].n_and_len);
+    chunk_len = plan_chunk_keys(a.plan[lo].request_and_chunk);
     const int32_t per_head = ceil_div(n * G, kRowsPerWg);
     if (per_head <= 0) return;
     const int32_t local = (int32_t)(blockIdx.x - mbase);

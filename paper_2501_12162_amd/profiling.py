@@ -4,6 +4,7 @@ Usage (on the GPU machine, after the runs named in each summary's header):
 
   python -m paper_2501_12162_amd.profiling stats  <kernel_stats.csv> <out.md> "<command>"
   python -m paper_2501_12162_amd.profiling traffic <fetch_dir> <write_dir> <workload> <out.json> "<commands>"
+  python -m paper_2501_12162_amd.profiling counters <out.json> <workload> "<commands>" <dir> [<dir> ...]
 
 ``traffic`` reads the per-dispatch FETCH_SIZE and WRITE_SIZE counters (KiB) of
 the tree-attention and argmax kernels, scales each by the factor that makes
@@ -27,7 +28,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CALIB_BYTES = 256 << 20
 
 
-_TRAFFIC_FILES = ("tree_attn.hip", "argmax.hip", "plan.h", "device_common.h")
+_TRAFFIC_FILES = ("tree_attn.hip", "argmax.hip", "plan.h", "device_common.h", "host_plan.h", "host_plan.cpp")
 
 
 def _block(text: str, start: str, end: str) -> str:
@@ -47,8 +48,8 @@ def _code_only(text: str) -> str:
 def kernel_source_hash() -> str:
     """sha256 over the sources that decide the measured kernels' traffic: the
     tree-attention and argmax kernels, their headers, the attention argument
-    block and the host planner and launch path (other entry points do not
-    change it)."""
+    block, the host validation and planner, and the launch path (other entry
+    points do not change it)."""
     h = hashlib.sha256()
     csrc = os.path.join(PKG, "csrc")
     for name in _TRAFFIC_FILES:
@@ -59,8 +60,7 @@ def kernel_source_hash() -> str:
         h.update(_code_only(_block(f.read(), "struct TreeAttnArgs", "};")).encode())
     with open(os.path.join(csrc, "adaserve.cpp")) as f:
         text = f.read()
-    h.update(_code_only(_block(text, "struct AttnShape", "// Beam step:")).encode())
-    h.update(_code_only(_block(text, "int32_t adaserve_tree_attn_verify(",
+    h.update(_code_only(_block(text, "int32_t tree_attn_verify_impl(",
                                      "int32_t adaserve_tree_accept(")).encode())
     return h.hexdigest()[:16]
 
@@ -134,6 +134,37 @@ def traffic_summary(fetch_dir: str, write_dir: str, workload: int, commands: str
     return res
 
 
+def counter_summary(dirs, workload: int, commands: str, simds: int = 1024) -> dict:
+    """Per-kernel medians over dispatches of every counter found under `dirs`
+    (one rocprofv3 --pmc run each), with derived figures for the attention
+    kernel: the matrix-core busy share SQ_VALU_MFMA_BUSY_CYCLES /
+    (GRBM_GUI_ACTIVE * SIMDs) and the bf16 matrix flops the hardware counted
+    (SQ_INSTS_VALU_MFMA_MOPS_BF16 * 512)."""
+    per = {}
+    for d in dirs:
+        files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        for f in files:
+            for r in csv.DictReader(open(f)):
+                kind = kernel_kind(r["Kernel_Name"])
+                if kind == "other":
+                    continue
+                per.setdefault(kind, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    res = {"workload": workload, "kernel_source_sha": kernel_source_hash(), "commands": commands,
+           "kernels": {}}
+    for kind, counters in per.items():
+        med = {c: statistics.median(v) for c, v in counters.items()}
+        k = {"counters": med, "dispatches": max(len(v) for v in counters.values())}
+        gui = med.get("GRBM_GUI_ACTIVE")
+        if gui and "SQ_VALU_MFMA_BUSY_CYCLES" in med:
+            k["mfma_busy_frac"] = med["SQ_VALU_MFMA_BUSY_CYCLES"] / (gui * simds)
+        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in med:
+            k["mfma_bf16_flops"] = med["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
+        if "SQ_INSTS_MFMA" in med and "SQ_INSTS_VALU" in med and med["SQ_INSTS_MFMA"]:
+            k["valu_per_mfma"] = (med["SQ_INSTS_VALU"] - med["SQ_INSTS_MFMA"]) / med["SQ_INSTS_MFMA"]
+        res["kernels"][kind] = k
+    return res
+
+
 def main(argv):
     if len(argv) >= 4 and argv[1] == "stats":
         md = stats_markdown(argv[2], argv[4] if len(argv) > 4 else "")
@@ -143,6 +174,12 @@ def main(argv):
     elif len(argv) >= 6 and argv[1] == "traffic":
         res = traffic_summary(argv[2], argv[3], int(argv[4]), argv[6] if len(argv) > 6 else "")
         with open(argv[5], "w") as f:
+            json.dump(res, f, indent=1)
+        print(json.dumps(res, indent=1))
+    elif len(argv) >= 5 and argv[1] == "counters":
+        # counters <out.json> <workload> "<commands>" <dir> [<dir> ...]
+        res = counter_summary(argv[5:], int(argv[3]), argv[4])
+        with open(argv[2], "w") as f:
             json.dump(res, f, indent=1)
         print(json.dumps(res, indent=1))
     else:
