@@ -129,6 +129,37 @@ int32_t adaserve_tree_attn_verify(int32_t num_requests, const int32_t *node_indp
                                   int32_t page_size, float sm_scale, int32_t dtype, void *out,
                                   void *workspace, size_t workspace_bytes, void *stream);
 
+/* Bytes of the static split-KV scratch of adaserve_tree_attn_verify_noalloc. */
+#define ADASERVE_TREE_ATTN_SCRATCH_BYTES (32u << 20)
+
+/*
+ * adaserve_tree_attn_verify without a workspace argument, for callers that
+ * cannot allocate device memory: code under HIP graph capture, serving loops
+ * that must not allocate, harnesses that forbid hipMalloc.  It calls no
+ * allocator of any kind.
+ *
+ * Arguments, layouts, results and errors are those of
+ * adaserve_tree_attn_verify (same plan, same kernels, bit-identical output);
+ * the split-KV partial results go to a static array of
+ * ADASERVE_TREE_ATTN_SCRATCH_BYTES bytes that the library holds on every
+ * device it runs on until the process ends.  A batch whose plan needs more
+ * than that (adaserve_tree_attn_workspace_bytes(...) > the limit) is
+ * rejected with ADASERVE_ERR_WORKSPACE before anything is enqueued.  Every
+ * call on one device shares that device's array: calls that overlap in time
+ * on one device (other streams, other threads) race and give undefined
+ * results; calls on one stream are ordered and safe.  The array's contents
+ * need no initialisation.
+ */
+int32_t adaserve_tree_attn_verify_noalloc(int32_t num_requests, const int32_t *node_indptr,
+                                          const int32_t *node_indptr_host, const int32_t *parent,
+                                          const void *q, const void *k_tree, const void *v_tree,
+                                          const void *k_pages, const void *v_pages, int32_t num_pages,
+                                          const int32_t *block_table, int32_t block_table_stride,
+                                          const int32_t *prefix_len, const int32_t *prefix_len_host,
+                                          int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                          int32_t page_size, float sm_scale, int32_t dtype, void *out,
+                                          void *stream);
+
 /*
  * Per-node vocabulary argmax of the verification logits (section 5.1: the
  * logits of every node come back from verification and the verified tokens

@@ -25,6 +25,7 @@ ADASERVE_ERR_DEVICE = 4
 ADASERVE_F32 = 0
 ADASERVE_BF16 = 1
 MAX_TREE_NODES = 128
+TREE_ATTN_SCRATCH_BYTES = 32 << 20
 
 _STATUS_NAMES = {1: "INVALID_ARGUMENT", 2: "UNSUPPORTED", 3: "WORKSPACE", 4: "DEVICE"}
 
@@ -34,6 +35,8 @@ SIGNATURES = {
     "adaserve_tree_attn_workspace_bytes": (_SZ, [_I32, _P, _P, _I32, _I32, _I32, _I32, _I32]),
     "adaserve_tree_attn_verify": (_I32, [_I32, _P, _P, _P, _P, _P, _P, _P, _P, _I32, _P, _I32, _P, _P,
                                          _I32, _I32, _I32, _I32, _F32, _I32, _P, _P, _SZ, _P]),
+    "adaserve_tree_attn_verify_noalloc": (_I32, [_I32, _P, _P, _P, _P, _P, _P, _P, _P, _I32, _P, _I32, _P,
+                                                 _P, _I32, _I32, _I32, _I32, _F32, _I32, _P, _P]),
     "adaserve_node_argmax": (_I32, [_P, _I64, _I32, _I32, _I32, _P, _P]),
     "adaserve_tree_accept": (_I32, [_I32, _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _P]),
     "adaserve_commit_accepted_kv": (_I32, [_I32, _P, _P, _P, _I32, _P, _P, _P, _P, _I32, _P, _I32, _P,
@@ -144,6 +147,25 @@ def adaserve_tree_attn_verify(*, node_indptr, node_indptr_host, parent, q, k_tre
         _dptr(v_tree), _dptr(k_pages), _dptr(v_pages), int(P), _dptr(block_table), int(bt_stride),
         _dptr(prefix_len), pl.ctypes.data, int(Hq), int(Hkv), int(D), int(ps), float(sm_scale),
         _dtype_code(q), _dptr(out), _dptr(workspace), int(ws_bytes), _stream(stream))
+    _check(st)
+
+
+def adaserve_tree_attn_verify_noalloc(*, node_indptr, node_indptr_host, parent, q, k_tree, v_tree,
+                                      k_pages, v_pages, block_table, prefix_len, prefix_len_host,
+                                      sm_scale: float, out, stream=None) -> None:
+    """Tree attention with the split-KV partials in the library's static
+    scratch (no workspace argument, nothing allocated); arguments as
+    ``adaserve_tree_attn_verify``."""
+    ip, pl = _host_i32(node_indptr_host), _host_i32(prefix_len_host)
+    T, Hq, D = q.shape
+    Hkv = k_tree.shape[1]
+    P, ps = k_pages.shape[0], k_pages.shape[2]
+    bt_stride = block_table.shape[1] if block_table.dim() == 2 else 0
+    st = load_library().adaserve_tree_attn_verify_noalloc(
+        int(pl.size), _dptr(node_indptr), ip.ctypes.data, _dptr(parent), _dptr(q), _dptr(k_tree),
+        _dptr(v_tree), _dptr(k_pages), _dptr(v_pages), int(P), _dptr(block_table), int(bt_stride),
+        _dptr(prefix_len), pl.ctypes.data, int(Hq), int(Hkv), int(D), int(ps), float(sm_scale),
+        _dtype_code(q), _dptr(out), _stream(stream))
     _check(st)
 
 

@@ -99,14 +99,15 @@ size_t adaserve_tree_attn_workspace_bytes(int32_t num_requests, const int32_t *n
 
 namespace {
 
-// The tree-attention entry point behind the C ABI.
+// Both tree-attention entry points: the caller's workspace, or (use_scratch)
+// the library's static per-device scratch array.
 int32_t tree_attn_verify_impl(int32_t num_requests, const int32_t *node_indptr, const int32_t *node_indptr_host,
                               const int32_t *parent, const void *q, const void *k_tree, const void *v_tree,
                               const void *k_pages, const void *v_pages, int32_t num_pages,
                               const int32_t *block_table, int32_t block_table_stride, const int32_t *prefix_len,
                               const int32_t *prefix_len_host, int32_t num_q_heads, int32_t num_kv_heads,
                               int32_t head_dim, int32_t page_size, float sm_scale, int32_t dtype, void *out,
-                              void *workspace, size_t workspace_bytes, void *stream) {
+                              void *workspace, size_t workspace_bytes, bool use_scratch, void *stream) {
   if (block_table_stride < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "block_table_stride < 0");
   if (num_pages < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_pages < 0");
   if (!std::isfinite(sm_scale)) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "sm_scale is not finite");
@@ -133,7 +134,13 @@ int32_t tree_attn_verify_impl(int32_t num_requests, const int32_t *node_indptr, 
     if (t && !aligned(t, 16)) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "tensor pointers must be 16-byte aligned");
   const AttnPlan plan =
       make_plan(num_requests, node_indptr_host, prefix_len_host, num_kv_heads, shape.group, head_dim, dtype);
-  if (plan.ws_bytes > 0) {
+  if (use_scratch) {
+    if (plan.ws_bytes > (size_t)ADASERVE_TREE_ATTN_SCRATCH_BYTES)
+      return fail(ADASERVE_ERR_WORKSPACE,
+                  "this batch needs %zu bytes of split-KV scratch; the static scratch holds %zu "
+                  "(call adaserve_tree_attn_verify with a workspace instead)",
+                  plan.ws_bytes, (size_t)ADASERVE_TREE_ATTN_SCRATCH_BYTES);
+  } else if (plan.ws_bytes > 0) {
     if (!workspace || workspace_bytes < plan.ws_bytes)
       return fail(ADASERVE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.ws_bytes,
                   workspace ? workspace_bytes : (size_t)0);
@@ -141,6 +148,10 @@ int32_t tree_attn_verify_impl(int32_t num_requests, const int32_t *node_indptr, 
   }
   st = check_device();
   if (st != ADASERVE_OK) return st;
+  if (use_scratch && plan.ws_bytes > 0) {
+    const hipError_t e = tree_attn_scratch(&workspace);
+    if (e != hipSuccess) return launch_status(e, "scratch address lookup");
+  }
 
   TreeAttnArgs a{};
   a.node_indptr = node_indptr;
@@ -201,7 +212,21 @@ int32_t adaserve_tree_attn_verify(int32_t num_requests, const int32_t *node_indp
   return tree_attn_verify_impl(num_requests, node_indptr, node_indptr_host, parent, q, k_tree, v_tree, k_pages,
                                v_pages, num_pages, block_table, block_table_stride, prefix_len, prefix_len_host,
                                num_q_heads, num_kv_heads, head_dim, page_size, sm_scale, dtype, out, workspace,
-                               workspace_bytes, stream);
+                               workspace_bytes, false, stream);
+}
+
+int32_t adaserve_tree_attn_verify_noalloc(int32_t num_requests, const int32_t *node_indptr,
+                                          const int32_t *node_indptr_host, const int32_t *parent, const void *q,
+                                          const void *k_tree, const void *v_tree, const void *k_pages,
+                                          const void *v_pages, int32_t num_pages, const int32_t *block_table,
+                                          int32_t block_table_stride, const int32_t *prefix_len,
+                                          const int32_t *prefix_len_host, int32_t num_q_heads,
+                                          int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
+                                          float sm_scale, int32_t dtype, void *out, void *stream) {
+  return tree_attn_verify_impl(num_requests, node_indptr, node_indptr_host, parent, q, k_tree, v_tree, k_pages,
+                               v_pages, num_pages, block_table, block_table_stride, prefix_len, prefix_len_host,
+                               num_q_heads, num_kv_heads, head_dim, page_size, sm_scale, dtype, out, nullptr, 0,
+                               true, stream);
 }
 
 int32_t adaserve_node_argmax(const void *logits, int64_t row_stride, int32_t num_rows, int32_t vocab, int32_t dtype,

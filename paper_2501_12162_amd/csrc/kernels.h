@@ -43,6 +43,10 @@ struct TreeAttnArgs {
 };
 
 hipError_t launch_tree_attn_bf16(TreeAttnArgs &a, int head_dim, bool needs_combine, hipStream_t stream);
+// Device address of the static split-KV scratch array on the current device
+// (ADASERVE_TREE_ATTN_SCRATCH_BYTES bytes, 256-byte aligned); looked up once
+// per device.
+hipError_t tree_attn_scratch(void **out);
 hipError_t launch_tree_attn_f32(const TreeAttnArgs &a, int head_dim, hipStream_t stream);
 
 hipError_t launch_node_argmax(const void *logits, int64_t row_stride, int32_t rows, int32_t vocab,

@@ -33,6 +33,7 @@
 #include <mutex>
 #include <type_traits>
 
+#include "adaserve.h"
 #include "device_common.h"
 #include "kernels.h"
 #include "plan.h"
@@ -933,6 +934,32 @@ __global__ __launch_bounds__(256) void tree_attn_f32_kernel(TreeAttnArgs a) {
 }
 
 }  // namespace
+
+// Split-KV partial results of adaserve_tree_attn_verify_noalloc, for callers
+// that cannot allocate: every call on a device shares that device's copy.
+// The kernels take its device address (from hipGetSymbolAddress, below) as
+// their workspace pointer, exactly like a caller's workspace; the array's
+// name is only a host-side stand-in and is never passed to a kernel.
+static __device__ __align__(256) unsigned char scratch[ADASERVE_TREE_ATTN_SCRATCH_BYTES];
+
+hipError_t tree_attn_scratch(void **out) {
+  static std::mutex mu;
+  static void *addr[256];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 256) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p || (uintptr_t)p % 256 != 0) return hipErrorInvalidValue;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
 
 // Device address of g_zero16 on the current device, looked up once per device.
 static hipError_t zero16_address(const void **out) {

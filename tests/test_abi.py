@@ -109,6 +109,32 @@ def test_verify_rejects_bad_arguments(lib, kw, code):
     assert lib.adaserve_last_error()
 
 
+def _verify_noalloc(lib, ip, pl, hq=8, hkv=2, d=128, scale=0.1, bt_stride=None):
+    ip = np.asarray(ip, np.int32)
+    pl = np.asarray(pl, np.int32)
+    if bt_stride is None:
+        bt_stride = max(1, int(-(-pl.max() // 16))) if pl.size else 1
+    return lib.adaserve_tree_attn_verify_noalloc(
+        int(pl.size), FAKE, ip.ctypes.data, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4, FAKE, bt_stride, FAKE,
+        pl.ctypes.data, hq, hkv, d, 16, scale, ada.ADASERVE_BF16, FAKE, None)
+
+
+def test_verify_noalloc_rejects_batches_past_the_scratch(lib):
+    # a plan needing more split-KV partials than the static scratch holds is
+    # refused before anything is enqueued, with the sizes in the message
+    ip = np.arange(0, 65 * 128, 128)
+    pl = np.full(64, 200000)
+    need = _ws(ip, pl, hq=8, hkv=2)
+    assert need > ada.TREE_ATTN_SCRATCH_BYTES
+    assert _verify_noalloc(lib, ip, pl) == ada.ADASERVE_ERR_WORKSPACE
+    msg = lib.adaserve_last_error()
+    assert b"scratch" in msg and str(need).encode() in msg
+    # and it validates like the workspace entry point
+    assert _verify_noalloc(lib, [0, 4], [20], hq=6, hkv=4) == ada.ADASERVE_ERR_INVALID_ARGUMENT
+    assert _verify_noalloc(lib, [0, 4], [20], scale=0.0) == ada.ADASERVE_ERR_UNSUPPORTED
+    assert _verify_noalloc(lib, [0, 4], [20], d=80) == ada.ADASERVE_ERR_UNSUPPORTED
+
+
 def test_verify_empty_batch_is_a_noop(lib):
     assert _verify(lib, ip=[0], pl=[]) == ada.ADASERVE_OK
 
