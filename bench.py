@@ -7,10 +7,12 @@ A step is one full verification pass over one batch: paged tree attention
 Inputs are seeded synthetic tensors shaped like the workload named by
 ``--workload`` (default: the long-context batch, 8 requests over 32768-token
 prefixes, the bandwidth-bound headline), resident in device memory before
-timing starts.  The three steps run one after another on one stream;
-``--overlap`` runs the per-node argmax (which reads only the logits) on a
-second stream of the same priority beside the attention, joined before the
-acceptance.  Consecutive steps cycle through several
+timing starts.  A step is one adaserve_tree_verify_step call (attention,
+argmax and acceptance in two launches: the argmax workgroups share the
+attention's grid); ``--unfused`` runs the three entry points one after
+another instead, and ``--unfused --overlap`` runs the per-node argmax (which
+reads only the logits) on a second stream of the same priority beside the
+attention, joined before the acceptance.  Consecutive steps cycle through several
 copies of the inputs so that no step finds its K/V or logits in the 256 MB
 last-level (MALL) cache left behind by the previous one.
 
@@ -40,8 +42,13 @@ def parse_args():
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--workload", type=int, default=5, choices=[1, 2, 3, 4, 5],
                    help="1 tiny-f32, 2 llama3-8b, 3 mixed-slo, 4 70b-shape, 5 long-context (default)")
+    p.add_argument("--unfused", action="store_true",
+                   help="time the step as three calls (attention, argmax, acceptance) instead of one")
+    p.add_argument("--no-parts", action="store_true",
+                   help="skip timing the step's parts alone (profiling runs: keeps the kernel statistics "
+                        "to the step's own launches)")
     p.add_argument("--overlap", action="store_true",
-                   help="run argmax on a second stream beside attention instead of after it")
+                   help="with --unfused: run argmax on a second stream beside attention instead of after it")
     p.add_argument("--mfma-workload", type=int, default=4, choices=[0, 1, 2, 3, 4, 5],
                    help="also time tree attention alone on this (matrix-core bound) workload and "
                         "report its MFMA fraction; 0 = skip")
@@ -237,11 +244,18 @@ def measured_traffic(workload: int, kernel: str):
         t = json.load(f)
     if t.get("kernel_source_sha") != kernel_source_hash():
         return None
+    if kernel == "tree_verify_step":
+        # the one-call step's two launches: the attention grid (with the
+        # argmax workgroups) and the merge grid (with the acceptance waves);
+        # a profile of separate argmax launches is not this step's
+        if "node_argmax" in t["kernels"]:
+            return None
+        kernel = "tree_attn"
     k = t["kernels"].get(kernel)
     if k is None:
         return None
     total = k["bytes"]
-    if kernel == "tree_attn" and "tree_attn_combine" in t["kernels"]:
+    if kernel in ("tree_attn", "tree_verify_step") and "tree_attn_combine" in t["kernels"]:
         total += t["kernels"]["tree_attn_combine"]["bytes"]
     return total
 
@@ -274,6 +288,25 @@ def attention_alone(n, calls=10):
             "hbm_frac": costs["attn_bytes"] / (mean * 1e-6) / 1e9 / HBM_PEAK_GBS,
             "alg_flops": costs["attn_flops"], "alg_bytes": costs["attn_bytes"],
             "traffic": measured_traffic(n, "tree_attn"), "calls": calls}
+
+
+def _finite(x):
+    """The JSON line with NaN / inf (parts not timed) written as null."""
+    if isinstance(x, dict):
+        return {k: _finite(v) for k, v in x.items()}
+    if isinstance(x, (list, tuple)):
+        return [_finite(v) for v in x]
+    if isinstance(x, float) and not math.isfinite(x):
+        return None
+    return x
+
+
+def hold_gpu(ms=3.0):
+    """Keeps the current stream busy for about `ms` (torch's bounded spin
+    kernel), so that calls enqueued after it are timed back to back on the
+    GPU rather than at the rate the host issues them."""
+    import torch
+    torch.cuda._sleep(int(ms * 2.4e6))
 
 
 def progress(msg):
@@ -312,24 +345,50 @@ def main():
     # argmax beside attention: a second stream of the default priority, forked
     # after the previous step's acceptance (which reads the argmax output)
     # and joined before this step's acceptance
-    side = torch.cuda.Stream() if args.overlap else None
+    side = torch.cuda.Stream() if (args.overlap and args.unfused) else None
     fork, join = torch.cuda.Event(), torch.cuda.Event()
+    fused = not args.unfused
 
-    def run_step(i, ev=None):
-        """One pass; `ev` = six timers around attention, argmax, acceptance."""
-        rp = reps[i % n_rep]
-        am = stream if side is None else side
-        if side is not None:
-            fork.record(stream)
-            side.wait_event(fork)
-        if ev is not None:
-            ev[0].record(stream)
+    def attention(rp):
         ada.adaserve_tree_attn_verify(
             node_indptr=dev.node_indptr, node_indptr_host=dev.node_indptr_host, parent=dev.parent,
             q=rp["q"], k_tree=rp["k_tree"], v_tree=rp["v_tree"], k_pages=rp["k_pages"],
             v_pages=rp["v_pages"], block_table=dev.block_table, prefix_len=dev.prefix_len,
             prefix_len_host=dev.prefix_len_host, sm_scale=b.sm_scale, out=dev.out,
             workspace=dev.workspace, stream=stream)
+
+    def accept(s):
+        ada.adaserve_tree_accept(node_indptr=dev.node_indptr, parent=dev.parent,
+                                 draft_tokens=dev.draft_tokens, target_argmax=dev.target_argmax,
+                                 max_accept=dev.max_accept, accept_len=dev.accept_len,
+                                 accept_tokens=dev.accept_tokens, accept_nodes=dev.accept_nodes,
+                                 stream=s)
+
+    def run_step(i, ev=None):
+        """One pass; `ev` = timers: two around the one-call step, or six
+        around attention, argmax and acceptance (--unfused)."""
+        rp = reps[i % n_rep]
+        if fused:
+            if ev is not None:
+                ev[0].record(stream)
+            ada.adaserve_tree_verify_step(
+                node_indptr=dev.node_indptr, node_indptr_host=dev.node_indptr_host, parent=dev.parent,
+                q=rp["q"], k_tree=rp["k_tree"], v_tree=rp["v_tree"], k_pages=rp["k_pages"],
+                v_pages=rp["v_pages"], block_table=dev.block_table, prefix_len=dev.prefix_len,
+                prefix_len_host=dev.prefix_len_host, sm_scale=b.sm_scale, logits=rp["logits"], vocab=b.vocab,
+                draft_tokens=dev.draft_tokens, max_accept=dev.max_accept, out=dev.out,
+                target_argmax=dev.target_argmax, accept_len=dev.accept_len, accept_tokens=dev.accept_tokens,
+                accept_nodes=dev.accept_nodes, workspace=dev.workspace, stream=stream)
+            if ev is not None:
+                ev[1].record(stream)
+            return
+        am = stream if side is None else side
+        if side is not None:
+            fork.record(stream)
+            side.wait_event(fork)
+        if ev is not None:
+            ev[0].record(stream)
+        attention(rp)
         if ev is not None:
             ev[1].record(stream)
             ev[2].record(am)
@@ -341,11 +400,7 @@ def main():
             stream.wait_event(join)
         if ev is not None:
             ev[4].record(stream)
-        ada.adaserve_tree_accept(node_indptr=dev.node_indptr, parent=dev.parent,
-                                 draft_tokens=dev.draft_tokens, target_argmax=dev.target_argmax,
-                                 max_accept=dev.max_accept, accept_len=dev.accept_len,
-                                 accept_tokens=dev.accept_tokens, accept_nodes=dev.accept_nodes,
-                                 stream=stream)
+        accept(stream)
         if ev is not None:
             ev[5].record(stream)
 
@@ -369,7 +424,7 @@ def main():
     # with the rocprofv3 kernel trace.
     n_inst = max(1, args.steps // EVENT_EVERY)
     sampled_steps = list(range(args.steps - n_inst, args.steps))
-    events = {i: [KernelTimer() for _ in range(6)] for i in sampled_steps}
+    events = {i: [KernelTimer() for _ in range(2 if fused else 6)] for i in sampled_steps}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -392,7 +447,7 @@ def main():
             block_table=dev.block_table, prefix_len=dev.prefix_len, new_prefix_len=new_len)
     commit()
     torch.cuda.synchronize()
-    calib_dst.copy_(calib_src)   # keeps the GPU busy while the host enqueues the timed calls
+    hold_gpu()   # the host enqueues every timed call before the GPU starts them
     commit_ev[0].record(stream)
     for _ in range(10):
         commit()
@@ -420,7 +475,7 @@ def main():
                                   tree_parent=s_par, tree_cand=s_cand)
     select()
     torch.cuda.synchronize()
-    calib_dst.copy_(calib_src)
+    hold_gpu()   # the host enqueues every timed call before the GPU starts them
     commit_ev[0].record(stream)
     for _ in range(10):
         select()
@@ -454,7 +509,7 @@ def main():
                                out_parent=b_par, out_token=b_tok, out_logprob=b_lp, workspace=beam_ws)
     beam(0)
     torch.cuda.synchronize()
-    calib_dst.copy_(calib_src)
+    hold_gpu()   # the host enqueues every timed call before the GPU starts them
     commit_ev[0].record(stream)
     for i in range(20):
         beam(i + 1)
@@ -488,7 +543,7 @@ def main():
                                          accept_tokens=s_tok, accept_nodes=s_nodes, workspace=s_ws)
     sampled()
     torch.cuda.synchronize()
-    calib_dst.copy_(calib_src)
+    hold_gpu()   # the host enqueues every timed call before the GPU starts them
     commit_ev[0].record(stream)
     for _ in range(10):
         sampled()
@@ -497,10 +552,33 @@ def main():
     sampled_us = commit_ev[0].elapsed_time(commit_ev[1]) * 1e3 / 10
     sampled_len = s_len.cpu().numpy()
 
-    attn_ms = np.array([e[0].elapsed_time(e[1]) for e in events.values()])
-    argmax_ms = np.array([e[2].elapsed_time(e[3]) for e in events.values()])
-    accept_ms = np.array([e[4].elapsed_time(e[5]) for e in events.values()])
-    step_ms = np.array([e[0].elapsed_time(e[5]) for e in events.values()])
+    if fused:
+        # the step's parts timed alone, call after call on the same inputs
+        # (each call's own events; the replicas keep the MALL cold)
+        step_ms = np.array([e[0].elapsed_time(e[1]) for e in events.values()])
+
+        def alone(fn, calls=10):
+            ev = [KernelTimer() for _ in range(calls + 1)]
+            torch.cuda.synchronize()
+            hold_gpu()   # the host enqueues every timed call before the GPU starts them
+            ev[0].record(stream)
+            for k in range(calls):
+                fn(reps[k % n_rep])
+                ev[k + 1].record(stream)
+            torch.cuda.synchronize()
+            return np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(calls)])
+        if args.no_parts:
+            attn_ms = argmax_ms = accept_ms = np.full(1, np.nan)
+        else:
+            attn_ms = alone(attention)
+            argmax_ms = alone(lambda rp: ada.adaserve_node_argmax(rp["logits"], b.vocab, dev.target_argmax,
+                                                                  stream=stream))
+            accept_ms = alone(lambda rp: accept(stream))
+    else:
+        attn_ms = np.array([e[0].elapsed_time(e[1]) for e in events.values()])
+        argmax_ms = np.array([e[2].elapsed_time(e[3]) for e in events.values()])
+        accept_ms = np.array([e[4].elapsed_time(e[5]) for e in events.values()])
+        step_ms = np.array([e[0].elapsed_time(e[5]) for e in events.values()])
 
     # sanity: the last step's argmax must equal the planted maxima
     got = dev.target_argmax.cpu().numpy()
@@ -527,7 +605,21 @@ def main():
     mfma_peak = BF16_MFMA_PEAK_TFLOPS if is_bf16 else FP32_PEAK_TFLOPS
     ridge = mfma_peak * 1e12 / (HBM_PEAK_GBS * 1e9)
     attn_ai = costs["attn_flops"] / costs["attn_bytes"]
-    if attn_us >= argmax_us:
+    step_bytes_alg = costs["attn_bytes"] + costs["argmax_bytes"] + costs["accept_bytes"]
+    if fused:
+        # the dominant unit is the one-call step (its two launches carry the
+        # attention, the argmax and the acceptance): all of its algorithmic
+        # bytes over the step call's event-timed duration
+        step_ai = costs["attn_flops"] / step_bytes_alg
+        if step_ai > ridge:
+            tf = costs["attn_flops"] / (step_us * 1e-6) / 1e12
+            roof = {"kernel": "tree_verify_step", "bound": "mfma", "achieved": tf, "peak": mfma_peak,
+                    "unit": "TFLOP/s", "frac": tf / mfma_peak}
+        else:
+            gbs = step_bytes_alg / (step_us * 1e-6) / 1e9
+            roof = {"kernel": "tree_verify_step", "bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS}
+    elif attn_us >= argmax_us:
         if attn_ai > ridge:
             roof = {"kernel": "tree_attn", "bound": "mfma", "achieved": attn_tflops, "peak": mfma_peak,
                     "unit": "TFLOP/s", "frac": attn_tflops / mfma_peak}
@@ -561,17 +653,21 @@ def main():
             "page_size": b.page_size, "vocab": b.vocab,
             "input_copies": n_rep,
             "instrumented_steps": len(sampled_steps),
-            "argmax_beside_attention": bool(args.overlap),
+            "step": "one adaserve_tree_verify_step call" if fused else
+                    "three calls (attention, argmax, acceptance)",
+            "argmax_beside_attention": bool(args.overlap and args.unfused),
         },
         "roofline": roof,
         "kernels": {
+            "step_us": step_us, "step_alg_bytes": step_bytes_alg,
+            "step_hbm_frac": step_bytes_alg / (step_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+            "parts_timed": "alone, call after call" if fused else "inside the timed steps",
             "tree_attn_us": attn_us, "tree_attn_hbm_frac": attn_gbs / HBM_PEAK_GBS,
             "tree_attn_mfma_frac": attn_tflops / mfma_peak, "tree_attn_ai_flop_per_byte": attn_ai,
             "tree_attn_alg_bytes": costs["attn_bytes"], "tree_attn_alg_flops": costs["attn_flops"],
             "node_argmax_us": argmax_us, "node_argmax_hbm_frac": argmax_gbs / HBM_PEAK_GBS,
             "node_argmax_alg_bytes": costs["argmax_bytes"],
             "tree_accept_us": accept_us,
-            "step_event_span_us": step_us,
             "kv_commit_us": commit_us,
             "kv_commit_rows": committed_rows,
             "kv_commit_bytes": committed_rows * 4 * b.num_kv_heads * b.head_dim * (2 if is_bf16 else 4),
@@ -582,8 +678,6 @@ def main():
             "beam_step_us": beam_us,
             "beam_step_rows": int(bb.logits.shape[0]),
             "beam_step_hbm_frac": beam_bytes / (beam_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
-            "path_hbm_frac": (costs["attn_bytes"] + costs["argmax_bytes"])
-            / (step_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
             "percentiles_us": {
                 name: {"p10": float(np.percentile(x, 10)) * 1e3, "p50": float(np.median(x)) * 1e3,
                        "p90": float(np.percentile(x, 90)) * 1e3}
@@ -600,7 +694,7 @@ def main():
     if not args.no_cpu_baseline:
         progress("oracle baseline on the host cores")
         line["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds)
-    print(json.dumps(line), flush=True)
+    print(json.dumps(_finite(line)), flush=True)
 
 
 if __name__ == "__main__":

@@ -14,6 +14,7 @@
  *   adaserve_node_argmax       the target's greedy choice at every node;
  *   adaserve_tree_accept       the longest accepted root path per request and
  *                              the tokens it commits;
+ *   adaserve_tree_verify_step  the three above as one call (two launches);
  *   adaserve_tree_accept_sampled  the same for sampled decoding (speculative
  *                              sampling over the tree);
  *   adaserve_commit_accepted_kv  the accepted path's keys and values written
@@ -203,6 +204,45 @@ int32_t adaserve_tree_accept(int32_t num_requests, int32_t total_nodes,
                              const int32_t *draft_tokens, const int32_t *target_argmax,
                              int32_t max_accept, int32_t *accept_len, int32_t *accept_tokens,
                              int32_t *accept_nodes, void *stream);
+
+/*
+ * The whole verification pass in one call (section 4.3 step 4: every tree
+ * of the batch scored in one pass, then the tokens to commit read off the
+ * node logits, section 5.1): tree attention as adaserve_tree_attn_verify,
+ * the per-node argmax as adaserve_node_argmax over the logits' T rows, and
+ * the acceptance as adaserve_tree_accept on that argmax.  Every output is
+ * bit-identical to those three calls in that order on the same stream.
+ *
+ * The attention arguments, workspace (size:
+ * adaserve_tree_attn_workspace_bytes) and limits are those of
+ * adaserve_tree_attn_verify; logits [T, logits_row_stride] have the
+ * attention's dtype (columns 0 .. vocab - 1 compared); draft_tokens [T],
+ * target_argmax [T], accept_len [num_requests], accept_tokens and
+ * accept_nodes [num_requests, max_accept] are as in adaserve_node_argmax
+ * and adaserve_tree_accept (all device memory).  Errors: the union of those
+ * calls' checks, all made before anything is enqueued.
+ *
+ * BF16 runs in two launches: the attention workgroups followed, in the same
+ * grid, by one argmax workgroup per node (they take the CUs no attention
+ * work unit holds and the attention's tail, so the logits stream beside the
+ * attention instead of after it); then the split-KV merge (when a prefix is
+ * split) together with one acceptance wave per request.  F32 enqueues the
+ * three calls' kernels one after another.  Calls that share a workspace
+ * must not overlap in time.
+ */
+int32_t adaserve_tree_verify_step(int32_t num_requests, const int32_t *node_indptr,
+                                  const int32_t *node_indptr_host, const int32_t *parent,
+                                  const void *q, const void *k_tree, const void *v_tree,
+                                  const void *k_pages, const void *v_pages, int32_t num_pages,
+                                  const int32_t *block_table, int32_t block_table_stride,
+                                  const int32_t *prefix_len, const int32_t *prefix_len_host,
+                                  int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                  int32_t page_size, float sm_scale, int32_t dtype,
+                                  const void *logits, int64_t logits_row_stride, int32_t vocab,
+                                  const int32_t *draft_tokens, int32_t max_accept, void *out,
+                                  int32_t *target_argmax, int32_t *accept_len,
+                                  int32_t *accept_tokens, int32_t *accept_nodes, void *workspace,
+                                  size_t workspace_bytes, void *stream);
 
 /*
  * Accepted-path KV commit: the keys and values of the accepted path enter

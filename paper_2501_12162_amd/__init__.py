@@ -37,6 +37,9 @@ SIGNATURES = {
                                          _I32, _I32, _I32, _I32, _F32, _I32, _P, _P, _SZ, _P]),
     "adaserve_tree_attn_verify_noalloc": (_I32, [_I32, _P, _P, _P, _P, _P, _P, _P, _P, _I32, _P, _I32, _P,
                                                  _P, _I32, _I32, _I32, _I32, _F32, _I32, _P, _P]),
+    "adaserve_tree_verify_step": (_I32, [_I32, _P, _P, _P, _P, _P, _P, _P, _P, _I32, _P, _I32, _P, _P,
+                                         _I32, _I32, _I32, _I32, _F32, _I32, _P, _I64, _I32, _P, _I32,
+                                         _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "adaserve_node_argmax": (_I32, [_P, _I64, _I32, _I32, _I32, _P, _P]),
     "adaserve_tree_accept": (_I32, [_I32, _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _P]),
     "adaserve_commit_accepted_kv": (_I32, [_I32, _P, _P, _P, _I32, _P, _P, _P, _P, _I32, _P, _I32, _P,
@@ -166,6 +169,29 @@ def adaserve_tree_attn_verify_noalloc(*, node_indptr, node_indptr_host, parent, 
         _dptr(v_tree), _dptr(k_pages), _dptr(v_pages), int(P), _dptr(block_table), int(bt_stride),
         _dptr(prefix_len), pl.ctypes.data, int(Hq), int(Hkv), int(D), int(ps), float(sm_scale),
         _dtype_code(q), _dptr(out), _stream(stream))
+    _check(st)
+
+
+def adaserve_tree_verify_step(*, node_indptr, node_indptr_host, parent, q, k_tree, v_tree, k_pages, v_pages,
+                              block_table, prefix_len, prefix_len_host, sm_scale: float, logits, vocab: int,
+                              draft_tokens, max_accept: int, out, target_argmax, accept_len, accept_tokens,
+                              accept_nodes, workspace=None, stream=None) -> None:
+    """Attention, argmax and acceptance of one verification pass in one call;
+    arguments as ``adaserve_tree_attn_verify``, ``adaserve_node_argmax`` and
+    ``adaserve_tree_accept`` (logits [T, row_stride])."""
+    ip, pl = _host_i32(node_indptr_host), _host_i32(prefix_len_host)
+    T, Hq, D = q.shape
+    Hkv = k_tree.shape[1]
+    P, ps = k_pages.shape[0], k_pages.shape[2]
+    bt_stride = block_table.shape[1] if block_table.dim() == 2 else 0
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = load_library().adaserve_tree_verify_step(
+        int(pl.size), _dptr(node_indptr), ip.ctypes.data, _dptr(parent), _dptr(q), _dptr(k_tree),
+        _dptr(v_tree), _dptr(k_pages), _dptr(v_pages), int(P), _dptr(block_table), int(bt_stride),
+        _dptr(prefix_len), pl.ctypes.data, int(Hq), int(Hkv), int(D), int(ps), float(sm_scale),
+        _dtype_code(q), _dptr(logits), int(logits.shape[1]), int(vocab), _dptr(draft_tokens), int(max_accept),
+        _dptr(out), _dptr(target_argmax), _dptr(accept_len), _dptr(accept_tokens), _dptr(accept_nodes),
+        _dptr(workspace), int(ws_bytes), _stream(stream))
     _check(st)
 
 

@@ -1,26 +1,11 @@
-// Longest-accepted-path acceptance on gfx950.
-//
-// One wavefront per request.  The tree (<= 128 nodes) is copied to LDS;
-// each lane walks the root paths of its two nodes to get their depth and
-// whether every node on the path matches (draft token == target argmax at
-// the parent); a wave-wide max over (depth, -id) of accepted nodes picks the
-// deepest accepted node with the smallest id; lanes then write the path and
-// its tokens.  Greedy tree verification per section 4.3 step 4, read with
-// section 2 (root = last generated token) and Algorithm 2's count of the
-// root as one accepted token.
-#include "device_common.h"
+// Longest-accepted-path acceptance on gfx950: one wavefront per request
+// (accept_wave.h).
+#include "accept_wave.h"
 #include "kernels.h"
-#include "plan.h"
 
 namespace adaserve {
 
 namespace {
-
-__device__ __forceinline__ int wave_max_int(int v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off, 64));
-  return v;
-}
 
 __global__ __launch_bounds__(64) void tree_accept_kernel(int32_t num_requests, int32_t total_nodes,
                                                          const int32_t *indptr, const int32_t *parent,
@@ -30,72 +15,8 @@ __global__ __launch_bounds__(64) void tree_accept_kernel(int32_t num_requests, i
   __shared__ int32_t par[kMaxTreeNodes], dr[kMaxTreeNodes], am[kMaxTreeNodes];
   const int r = blockIdx.x;
   if (r >= num_requests) return;
-  const int lane = threadIdx.x;
-  int32_t *tok_row = accept_tokens + (int64_t)r * max_accept;
-  int32_t *node_row = accept_nodes + (int64_t)r * max_accept;
-
-  const int32_t a0 = indptr[r], a1 = indptr[r + 1];
-  const int32_t n = a1 - a0;
-  bool ok = a0 >= 0 && a1 <= total_nodes && n >= 1 && n <= kMaxTreeNodes;
-  if (ok) {
-    for (int i = lane; i < n; i += 64) {
-      par[i] = parent[a0 + i];
-      dr[i] = draft[a0 + i];
-      am[i] = amax[a0 + i];
-    }
-  }
-  __syncthreads();
-  int bad = 0;
-  if (ok) {
-    for (int i = lane; i < n; i += 64) {
-      const int p = par[i];
-      bad |= (i == 0) ? (p != -1) : (p < 0 || p >= i);
-    }
-  }
-  ok = ok && wave_max_int(bad) == 0;
-
-  // Depth and acceptance of every node; key = (depth << 8) | (255 - id).
-  int deepest = 0, best = -1;
-  if (ok) {
-    for (int i = lane; i < n; i += 64) {
-      int v = i, d = 0;
-      bool acc = true;
-      while (v != 0) {
-        const int p = par[v];
-        acc = acc && dr[v] == am[p];
-        v = p;
-        ++d;
-      }
-      deepest = max(deepest, d);
-      if (acc) best = max(best, (d << 8) | (255 - i));
-    }
-  }
-  deepest = wave_max_int(deepest);
-  best = wave_max_int(best);
-  ok = ok && deepest < max_accept;
-
-  if (!ok) {
-    for (int k = lane; k < max_accept; k += 64) {
-      tok_row[k] = -1;
-      node_row[k] = -1;
-    }
-    if (lane == 0) accept_len[r] = -1;
-    return;
-  }
-  const int dstar = best >> 8;
-  const int istar = 255 - (best & 255);
-  for (int k = lane; k < max_accept; k += 64) {
-    int node = -1, token = -1;
-    if (k <= dstar) {
-      int child = istar;  // path node at depth k+1 (or i* itself when k == d*)
-      for (int s = 0; s < dstar - k - 1; ++s) child = par[child];
-      node = (k == dstar) ? istar : par[child];
-      token = (k == dstar) ? am[istar] : dr[child];
-    }
-    tok_row[k] = token;
-    node_row[k] = node;
-  }
-  if (lane == 0) accept_len[r] = dstar + 1;
+  accept_request(r, total_nodes, indptr, parent, draft, amax, max_accept, accept_len, accept_tokens,
+                 accept_nodes, par, dr, am);
 }
 
 }  // namespace

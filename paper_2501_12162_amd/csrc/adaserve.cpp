@@ -99,15 +99,50 @@ size_t adaserve_tree_attn_workspace_bytes(int32_t num_requests, const int32_t *n
 
 namespace {
 
-// Both tree-attention entry points: the caller's workspace, or (use_scratch)
-// the library's static per-device scratch array.
+// The argmax and acceptance arguments of the whole verification step.
+struct StepArgs {
+  const void *logits;
+  int64_t row_stride;
+  int32_t vocab;
+  const int32_t *draft_tokens;
+  int32_t max_accept;
+  int32_t *target_argmax;
+  int32_t *accept_len;
+  int32_t *accept_tokens;
+  int32_t *accept_nodes;
+};
+
+// Host checks of the step's argmax and acceptance arguments (the attention
+// arguments are checked by tree_attn_verify_impl).
+int32_t validate_step(const StepArgs &st, int32_t num_requests, int32_t total_nodes, int32_t dtype) {
+  if (st.max_accept < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "max_accept %d < 1", st.max_accept);
+  if ((int64_t)num_requests * st.max_accept > INT32_MAX)
+    return fail(ADASERVE_ERR_UNSUPPORTED, "num_requests * max_accept exceeds 2^31 - 1");
+  if (st.vocab < 1) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "vocab %d < 1", st.vocab);
+  if (st.row_stride < st.vocab)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "row_stride %lld < vocab %d", (long long)st.row_stride, st.vocab);
+  if (num_requests == 0) return ADASERVE_OK;
+  if (!st.accept_len || !st.accept_tokens || !st.accept_nodes || !st.target_argmax)
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  if (total_nodes > 0 && (!st.logits || !st.draft_tokens))
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  const size_t esz = dtype == ADASERVE_BF16 ? 2 : 4;
+  if (!aligned(st.logits, esz) || !aligned(st.target_argmax, 4))
+    return fail(ADASERVE_ERR_INVALID_ARGUMENT, "misaligned logits or argmax pointer");
+  return ADASERVE_OK;
+}
+
+// The tree-attention entry points and the verification step: the caller's
+// workspace, or (use_scratch) the library's static per-device scratch array;
+// with `step`, the argmax and acceptance of the same pass are enqueued too.
 int32_t tree_attn_verify_impl(int32_t num_requests, const int32_t *node_indptr, const int32_t *node_indptr_host,
                               const int32_t *parent, const void *q, const void *k_tree, const void *v_tree,
                               const void *k_pages, const void *v_pages, int32_t num_pages,
                               const int32_t *block_table, int32_t block_table_stride, const int32_t *prefix_len,
                               const int32_t *prefix_len_host, int32_t num_q_heads, int32_t num_kv_heads,
                               int32_t head_dim, int32_t page_size, float sm_scale, int32_t dtype, void *out,
-                              void *workspace, size_t workspace_bytes, bool use_scratch, void *stream) {
+                              void *workspace, size_t workspace_bytes, bool use_scratch, const StepArgs *step,
+                              void *stream) {
   if (block_table_stride < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "block_table_stride < 0");
   if (num_pages < 0) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "num_pages < 0");
   if (!std::isfinite(sm_scale)) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "sm_scale is not finite");
@@ -119,6 +154,10 @@ int32_t tree_attn_verify_impl(int32_t num_requests, const int32_t *node_indptr, 
   // scores in raw units, which orders them only for a positive scale
   if (dtype == ADASERVE_BF16 && !(sm_scale > 0.f))
     return fail(ADASERVE_ERR_UNSUPPORTED, "sm_scale %g: the BF16 path needs sm_scale > 0", (double)sm_scale);
+  if (step) {
+    st = validate_step(*step, num_requests, shape.total_nodes, dtype);
+    if (st != ADASERVE_OK) return st;
+  }
   if (num_requests == 0) return ADASERVE_OK;
   if (!node_indptr || !parent || !q || !k_tree || !v_tree || !out || !prefix_len)
     return fail(ADASERVE_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
@@ -192,9 +231,34 @@ int32_t tree_attn_verify_impl(int32_t num_requests, const int32_t *node_indptr, 
   a.sm_scale = sm_scale;
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   hipStream_t s = (hipStream_t)stream;
-  if (dtype == ADASERVE_BF16)
-    return launch_status(launch_tree_attn_bf16(a, head_dim, plan.needs_combine, s), "tree attention launch");
-  return launch_status(launch_tree_attn_f32(a, head_dim, s), "tree attention launch");
+  if (step && dtype == ADASERVE_BF16) {
+    a.logits = step->logits;
+    a.logit_stride = step->row_stride;
+    a.vocab = step->vocab;
+    a.argmax_rows = shape.total_nodes;
+    a.argmax_out = step->target_argmax;
+    a.draft_tokens = step->draft_tokens;
+    a.max_accept = step->max_accept;
+    a.accept_requests = num_requests;
+    a.accept_len = step->accept_len;
+    a.accept_tokens = step->accept_tokens;
+    a.accept_nodes = step->accept_nodes;
+    return launch_status(launch_verify_step_bf16(a, head_dim, plan.needs_combine, s), "verification step launch");
+  }
+  if (dtype == ADASERVE_BF16) {
+    st = launch_status(launch_tree_attn_bf16(a, head_dim, plan.needs_combine, s), "tree attention launch");
+  } else {
+    st = launch_status(launch_tree_attn_f32(a, head_dim, s), "tree attention launch");
+  }
+  if (st != ADASERVE_OK || !step) return st;
+  st = launch_status(launch_node_argmax(step->logits, step->row_stride, shape.total_nodes, step->vocab,
+                                        dtype == ADASERVE_BF16, step->target_argmax, s),
+                     "argmax launch");
+  if (st != ADASERVE_OK) return st;
+  return launch_status(launch_tree_accept(num_requests, shape.total_nodes, node_indptr, parent, step->draft_tokens,
+                                          step->target_argmax, step->max_accept, step->accept_len,
+                                          step->accept_tokens, step->accept_nodes, s),
+                       "accept launch");
 }
 
 }  // namespace
@@ -212,7 +276,7 @@ int32_t adaserve_tree_attn_verify(int32_t num_requests, const int32_t *node_indp
   return tree_attn_verify_impl(num_requests, node_indptr, node_indptr_host, parent, q, k_tree, v_tree, k_pages,
                                v_pages, num_pages, block_table, block_table_stride, prefix_len, prefix_len_host,
                                num_q_heads, num_kv_heads, head_dim, page_size, sm_scale, dtype, out, workspace,
-                               workspace_bytes, false, stream);
+                               workspace_bytes, false, nullptr, stream);
 }
 
 int32_t adaserve_tree_attn_verify_noalloc(int32_t num_requests, const int32_t *node_indptr,
@@ -226,7 +290,25 @@ int32_t adaserve_tree_attn_verify_noalloc(int32_t num_requests, const int32_t *n
   return tree_attn_verify_impl(num_requests, node_indptr, node_indptr_host, parent, q, k_tree, v_tree, k_pages,
                                v_pages, num_pages, block_table, block_table_stride, prefix_len, prefix_len_host,
                                num_q_heads, num_kv_heads, head_dim, page_size, sm_scale, dtype, out, nullptr, 0,
-                               true, stream);
+                               true, nullptr, stream);
+}
+
+int32_t adaserve_tree_verify_step(int32_t num_requests, const int32_t *node_indptr, const int32_t *node_indptr_host,
+                                  const int32_t *parent, const void *q, const void *k_tree, const void *v_tree,
+                                  const void *k_pages, const void *v_pages, int32_t num_pages,
+                                  const int32_t *block_table, int32_t block_table_stride, const int32_t *prefix_len,
+                                  const int32_t *prefix_len_host, int32_t num_q_heads, int32_t num_kv_heads,
+                                  int32_t head_dim, int32_t page_size, float sm_scale, int32_t dtype,
+                                  const void *logits, int64_t logits_row_stride, int32_t vocab,
+                                  const int32_t *draft_tokens, int32_t max_accept, void *out, int32_t *target_argmax,
+                                  int32_t *accept_len, int32_t *accept_tokens, int32_t *accept_nodes,
+                                  void *workspace, size_t workspace_bytes, void *stream) {
+  const StepArgs step{logits, logits_row_stride, vocab, draft_tokens, max_accept, target_argmax, accept_len,
+                      accept_tokens, accept_nodes};
+  return tree_attn_verify_impl(num_requests, node_indptr, node_indptr_host, parent, q, k_tree, v_tree, k_pages,
+                               v_pages, num_pages, block_table, block_table_stride, prefix_len, prefix_len_host,
+                               num_q_heads, num_kv_heads, head_dim, page_size, sm_scale, dtype, out, workspace,
+                               workspace_bytes, false, &step, stream);
 }
 
 int32_t adaserve_node_argmax(const void *logits, int64_t row_stride, int32_t num_rows, int32_t vocab, int32_t dtype,

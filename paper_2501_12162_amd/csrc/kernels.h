@@ -38,11 +38,28 @@ struct TreeAttnArgs {
   int64_t merge_blocks;        // workgroups of the split-KV merge
   float sm_scale;
   float scale_log2;            // sm_scale * log2(e)
+  // Fused verification step (adaserve_tree_verify_step; zero counts
+  // otherwise): argmax_rows argmax workgroups follow the attention grid, and
+  // acceptance waves for accept_requests requests follow the merge grid.
+  const void *logits;          // [argmax_rows, logit_stride] bf16
+  int64_t logit_stride;
+  int32_t vocab;
+  int32_t argmax_rows;
+  int32_t *argmax_out;         // [argmax_rows]
+  const int32_t *draft_tokens; // [total_nodes]
+  int32_t max_accept;
+  int32_t accept_requests;
+  int32_t *accept_len;         // [num_requests]
+  int32_t *accept_tokens;      // [num_requests, max_accept]
+  int32_t *accept_nodes;       // [num_requests, max_accept]
   int32_t plan_count;          // entries used in plan[] (0: scan the device arrays)
   PlanEntry plan[kPlanMax];
 };
 
 hipError_t launch_tree_attn_bf16(TreeAttnArgs &a, int head_dim, bool needs_combine, hipStream_t stream);
+// The verification step in two launches: attention + argmax workgroups, then
+// the split-KV merge (when a prefix is split) + acceptance waves.
+hipError_t launch_verify_step_bf16(TreeAttnArgs &a, int head_dim, bool needs_combine, hipStream_t stream);
 // Device address of the static split-KV scratch array on the current device
 // (ADASERVE_TREE_ATTN_SCRATCH_BYTES bytes, 256-byte aligned); looked up once
 // per device.

@@ -33,7 +33,9 @@
 #include <mutex>
 #include <type_traits>
 
+#include "accept_wave.h"
 #include "adaserve.h"
+#include "argmax_row.h"
 #include "device_common.h"
 #include "kernels.h"
 #include "plan.h"
@@ -190,6 +192,15 @@ __global__ __launch_bounds__(kThreads, 2) void tree_attn_bf16_kernel(TreeAttnArg
   uint32_t *const anc = (uint32_t *)(ring + (NST - 1) * 2 * BLK + BLK + kMaxTreeNodes * 4);
   static_assert(kMaxTreeNodes * 4 * 5 <= BLK, "parents and ancestor sets fit in a V half-stage");
 
+  if ((int64_t)blockIdx.x >= a.padded_grid) {
+    // fused verification step: argmax workgroups follow the attention units,
+    // taking CUs that no attention unit occupies
+    const int64_t row = (int64_t)blockIdx.x - a.padded_grid;
+    if (row < a.argmax_rows)
+      argmax_row<true, kThreads>(a.logits, a.logit_stride, a.vocab, (int32_t)row, a.argmax_out, (float *)ring,
+                                 (int *)(ring + 64));
+    return;
+  }
   const int64_t uid = xcd_swizzle(blockIdx.x, a.padded_grid);
   if (uid >= a.units) return;
   int32_t r, node_base, n, L, chunk_len;
@@ -702,7 +713,17 @@ __global__ __launch_bounds__(kThreads) void tree_attn_combine_kernel(TreeAttnArg
   constexpr int kRowsPerWg = 16;
   constexpr int TPR = kThreads / kRowsPerWg;  // threads per row
   constexpr int CPT = D / TPR;                // columns per thread (8 or 4)
-  if ((int64_t)blockIdx.x >= a.merge_blocks) return;
+  if ((int64_t)blockIdx.x >= a.merge_blocks) {
+    // fused verification step: one acceptance wave per request after the
+    // merge workgroups (the argmax finished in the previous launch)
+    __shared__ int32_t acc_lds[kThreads / 64][3][kMaxTreeNodes];
+    const int w = threadIdx.x >> 6;
+    const int64_t r = ((int64_t)blockIdx.x - a.merge_blocks) * (kThreads / 64) + w;
+    if (r < a.accept_requests)
+      accept_request((int)r, a.total_nodes, a.node_indptr, a.parent, a.draft_tokens, a.argmax_out, a.max_accept,
+                     a.accept_len, a.accept_tokens, a.accept_nodes, acc_lds[w][0], acc_lds[w][1], acc_lds[w][2]);
+    return;
+  }
   int32_t node_base, n, L, chunk_len, tile, g, rl;
   int64_t ubase;
   const int G = a.group, RT = a.rows_per_tile;
@@ -996,6 +1017,30 @@ hipError_t launch_tree_attn_bf16(TreeAttnArgs &a, int head_dim, bool needs_combi
     hipLaunchKernelGGL(tree_attn_combine_kernel<128>, cgrid, block, 0, stream, a);
   else
     hipLaunchKernelGGL(tree_attn_combine_kernel<64>, cgrid, block, 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_verify_step_bf16(TreeAttnArgs &a, int head_dim, bool needs_combine, hipStream_t stream) {
+  hipError_t e = zero16_address(&a.zero16);
+  if (e != hipSuccess) return e;
+  const dim3 block(kThreads);
+  const int64_t g1 = (a.units > 0 ? a.padded_grid : 0) + a.argmax_rows;
+  if (a.units == 0) a.padded_grid = 0;
+  if (g1 > 0) {
+    if (head_dim == 128)
+      hipLaunchKernelGGL(tree_attn_bf16_kernel<128>, dim3((unsigned)g1), block, 0, stream, a);
+    else
+      hipLaunchKernelGGL(tree_attn_bf16_kernel<64>, dim3((unsigned)g1), block, 0, stream, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (!needs_combine) a.merge_blocks = 0;
+  const int64_t g2 = a.merge_blocks + (a.accept_requests + kThreads / 64 - 1) / (kThreads / 64);
+  if (g2 == 0) return hipSuccess;
+  if (head_dim == 128)
+    hipLaunchKernelGGL(tree_attn_combine_kernel<128>, dim3((unsigned)g2), block, 0, stream, a);
+  else
+    hipLaunchKernelGGL(tree_attn_combine_kernel<64>, dim3((unsigned)g2), block, 0, stream, a);
   return hipGetLastError();
 }
 

@@ -12,7 +12,7 @@ import numpy as np
 
 from . import (ADASERVE_BF16, ADASERVE_F32, MAX_TREE_NODES, adaserve_node_argmax,
                adaserve_tree_accept, adaserve_tree_attn_verify,
-               adaserve_tree_attn_workspace_bytes)
+               adaserve_tree_attn_workspace_bytes, adaserve_tree_verify_step)
 
 
 def to_device(a: np.ndarray, dtype: str, device):
@@ -78,10 +78,21 @@ class DeviceBatch:
                              stream=stream)
 
     def step(self, stream=None) -> None:
-        """One verification pass: attention, argmax, acceptance."""
+        """One verification pass: attention, argmax, acceptance (three calls)."""
         self.attention(stream)
         self.argmax(stream)
         self.accept(stream)
+
+    def fused_step(self, stream=None) -> None:
+        """The same pass through adaserve_tree_verify_step (one call)."""
+        adaserve_tree_verify_step(
+            node_indptr=self.node_indptr, node_indptr_host=self.node_indptr_host, parent=self.parent,
+            q=self.q, k_tree=self.k_tree, v_tree=self.v_tree, k_pages=self.k_pages, v_pages=self.v_pages,
+            block_table=self.block_table, prefix_len=self.prefix_len, prefix_len_host=self.prefix_len_host,
+            sm_scale=self.batch.sm_scale, logits=self.logits, vocab=self.batch.vocab,
+            draft_tokens=self.draft_tokens, max_accept=self.max_accept, out=self.out,
+            target_argmax=self.target_argmax, accept_len=self.accept_len, accept_tokens=self.accept_tokens,
+            accept_nodes=self.accept_nodes, workspace=self.workspace, stream=stream)
 
     def results(self):
         """Host copies: (out as float32 ndarray, argmax, accept_len, tokens, nodes)."""

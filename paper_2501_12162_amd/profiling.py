@@ -134,12 +134,24 @@ def traffic_summary(fetch_dir: str, write_dir: str, workload: int, commands: str
     return res
 
 
-def counter_summary(dirs, workload: int, commands: str, simds: int = 1024) -> dict:
+def counter_summary(dirs, workload: int, commands: str, simds: int = 1024, xcds: int = 8) -> dict:
     """Per-kernel medians over dispatches of every counter found under `dirs`
-    (one rocprofv3 --pmc run each), with derived figures for the attention
-    kernel: the matrix-core busy share SQ_VALU_MFMA_BUSY_CYCLES /
-    (GRBM_GUI_ACTIVE * SIMDs) and the bf16 matrix flops the hardware counted
-    (SQ_INSTS_VALU_MFMA_MOPS_BF16 * 512)."""
+    (one rocprofv3 --pmc run each), with derived figures:
+
+    * rocprofv3 reports each counter summed over its hardware instances, so
+      GRBM_GUI_ACTIVE is the sum over the XCDs: active cycles per XCD =
+      GRBM_GUI_ACTIVE / xcds, and that over the dispatch's duration is the
+      clock the kernel ran at;
+    * mfma_busy_frac = SQ_VALU_MFMA_BUSY_CYCLES / (cycles per XCD * SIMDs),
+      the share of SIMD-cycles the matrix cores were busy;
+    * mfma_bf16_flops = SQ_INSTS_VALU_MFMA_MOPS_BF16 * 512, the bf16 matrix
+      work the hardware counted (padding and row-sum products included);
+    * valu_per_mfma, the non-matrix vector instructions per matrix one;
+    * lds_conflict_frac = SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE, the share
+      of LDS cycles lost to bank conflicts;
+    * wait / active shares of SQ_WAVE_CYCLES (SQ_WAIT_ANY: waits on memory
+      counters and barriers; SQ_WAIT_INST_ANY: waiting to issue;
+      SQ_ACTIVE_INST_ANY: issuing), all in the same units."""
     per = {}
     for d in dirs:
         files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
@@ -148,19 +160,33 @@ def counter_summary(dirs, workload: int, commands: str, simds: int = 1024) -> di
                 kind = kernel_kind(r["Kernel_Name"])
                 if kind == "other":
                     continue
-                per.setdefault(kind, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+                c = per.setdefault(kind, {})
+                c.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+                if r.get("Start_Timestamp") and r.get("End_Timestamp"):
+                    c.setdefault("duration_ns", []).append(float(r["End_Timestamp"]) - float(r["Start_Timestamp"]))
     res = {"workload": workload, "kernel_source_sha": kernel_source_hash(), "commands": commands,
            "kernels": {}}
     for kind, counters in per.items():
         med = {c: statistics.median(v) for c, v in counters.items()}
         k = {"counters": med, "dispatches": max(len(v) for v in counters.values())}
         gui = med.get("GRBM_GUI_ACTIVE")
+        if gui:
+            k["cycles_per_xcd"] = gui / xcds
+            if med.get("duration_ns"):
+                k["clock_ghz"] = gui / xcds / med["duration_ns"]
         if gui and "SQ_VALU_MFMA_BUSY_CYCLES" in med:
-            k["mfma_busy_frac"] = med["SQ_VALU_MFMA_BUSY_CYCLES"] / (gui * simds)
+            k["mfma_busy_frac"] = med["SQ_VALU_MFMA_BUSY_CYCLES"] / (gui / xcds * simds)
         if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in med:
             k["mfma_bf16_flops"] = med["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
         if "SQ_INSTS_MFMA" in med and "SQ_INSTS_VALU" in med and med["SQ_INSTS_MFMA"]:
             k["valu_per_mfma"] = (med["SQ_INSTS_VALU"] - med["SQ_INSTS_MFMA"]) / med["SQ_INSTS_MFMA"]
+        if med.get("SQ_LDS_IDX_ACTIVE"):
+            k["lds_conflict_frac"] = med.get("SQ_LDS_BANK_CONFLICT", 0.0) / med["SQ_LDS_IDX_ACTIVE"]
+        if med.get("SQ_WAVE_CYCLES"):
+            for name, key in (("SQ_WAIT_ANY", "wait_any_frac"), ("SQ_WAIT_INST_ANY", "wait_inst_frac"),
+                              ("SQ_ACTIVE_INST_ANY", "active_inst_frac")):
+                if name in med:
+                    k[key] = med[name] / med["SQ_WAVE_CYCLES"]
         res["kernels"][kind] = k
     return res
 

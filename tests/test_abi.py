@@ -135,6 +135,48 @@ def test_verify_noalloc_rejects_batches_past_the_scratch(lib):
     assert _verify_noalloc(lib, [0, 4], [20], d=80) == ada.ADASERVE_ERR_UNSUPPORTED
 
 
+def _step(lib, **kw):
+    ip = np.asarray(kw.pop("ip", [0, 4]), np.int32)
+    pl = np.asarray(kw.pop("pl", [20]), np.int32)
+    args = dict(scale=0.1, dtype=ada.ADASERVE_BF16, hq=8, hkv=2, d=128, logits=FAKE, stride=1000, vocab=1000,
+                draft=FAKE, max_accept=8, out=FAKE, amax=FAKE, alen=FAKE, atok=FAKE, anodes=FAKE, ws=None,
+                ws_bytes=0, q=FAKE)
+    args.update(kw)
+    return lib.adaserve_tree_verify_step(
+        int(pl.size), FAKE, ip.ctypes.data, FAKE, args["q"], FAKE, FAKE, FAKE, FAKE, 4, FAKE, 2, FAKE,
+        pl.ctypes.data, args["hq"], args["hkv"], args["d"], 16, args["scale"], args["dtype"], args["logits"],
+        args["stride"], args["vocab"], args["draft"], args["max_accept"], args["out"], args["amax"], args["alen"],
+        args["atok"], args["anodes"], args["ws"], args["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(hq=6, hkv=4), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(scale=0.0), ada.ADASERVE_ERR_UNSUPPORTED),
+    (dict(vocab=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(stride=999), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(max_accept=0), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(logits=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(logits=FAKE + 1), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(draft=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(amax=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(amax=FAKE + 2), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(alen=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(atok=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(anodes=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(out=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(q=FAKE + 2), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+    (dict(ip=[0, 32], pl=[32768]), ada.ADASERVE_ERR_INVALID_ARGUMENT),   # block table too narrow
+    (dict(dtype=ada.ADASERVE_F32, logits=FAKE + 2), ada.ADASERVE_ERR_INVALID_ARGUMENT),
+])
+def test_verify_step_rejects_bad_arguments(lib, kw, code):
+    assert _step(lib, **kw) == code
+    assert lib.adaserve_last_error()
+
+
+def test_verify_step_empty_batch_is_a_noop(lib):
+    assert _step(lib, ip=[0], pl=[]) == ada.ADASERVE_OK
+
+
 def test_verify_empty_batch_is_a_noop(lib):
     assert _verify(lib, ip=[0], pl=[]) == ada.ADASERVE_OK
 
