@@ -234,24 +234,24 @@ def cpu_baseline(b, budget_s, one_thread=True):
 
 def measured_traffic(workload: int, kernel: str):
     """HBM bytes per launch of `kernel` from the committed counter summary,
-    or None when there is none or the kernel sources changed since."""
+    or None when there is none or the kernel sources changed since.  The
+    one-call step ("tree_verify_step": its two launches) is profiled in
+    profiles/traffic_workload<N>.json; the attention call alone
+    ("tree_attn": main kernel + split-KV merge) and the standalone argmax in
+    profiles/traffic_attention_workload<N>.json (a --unfused run)."""
     from paper_2501_12162_amd.profiling import kernel_source_hash
-    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
-                        "traffic_workload%d.json" % workload)
+    name = "traffic_workload%d.json" if kernel == "tree_verify_step" else "traffic_attention_workload%d.json"
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", name % workload)
     if not os.path.exists(path):
         return None
     with open(path) as f:
         t = json.load(f)
     if t.get("kernel_source_sha") != kernel_source_hash():
         return None
-    if kernel == "tree_verify_step":
-        # the one-call step's two launches: the attention grid (with the
-        # argmax workgroups) and the merge grid (with the acceptance waves);
-        # a profile of separate argmax launches is not this step's
-        if "node_argmax" in t["kernels"]:
-            return None
-        kernel = "tree_attn"
-    k = t["kernels"].get(kernel)
+    fused_profile = "node_argmax" not in t["kernels"]
+    if fused_profile != (kernel == "tree_verify_step"):
+        return None
+    k = t["kernels"].get("tree_attn" if kernel == "tree_verify_step" else kernel)
     if k is None:
         return None
     total = k["bytes"]
