@@ -112,6 +112,14 @@ def test_llama_shape_with_unused_beams(torch_cuda):
     assert check(torch_cuda, b.logits, b.vocab, b.beam_logprob, 8, "bf16") > 100
 
 
+def test_long_context_batch_shape(torch_cuda):
+    """8 requests x 8 beams over 128256 tokens (the long-context batch's
+    beam step: 64 rows, two scan workgroups per row)."""
+    rng = np.random.Generator(np.random.PCG64(4))
+    b = make_beam_batch(rng, 8, 8, 128256)
+    assert check(torch_cuda, b.logits, b.vocab, b.beam_logprob, 8, "bf16") > 50
+
+
 def test_qwen_vocab_padded_rows(torch_cuda):
     rng = np.random.Generator(np.random.PCG64(3))
     b = make_beam_batch(rng, 4, 4, 151936, row_pad=64)
