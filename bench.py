@@ -52,6 +52,9 @@ def parse_args():
     p.add_argument("--mfma-workload", type=int, default=4, choices=[0, 1, 2, 3, 4, 5],
                    help="also time tree attention alone on this (matrix-core bound) workload and "
                         "report its MFMA fraction; 0 = skip")
+    p.add_argument("--tp-share", type=int, default=4,
+                   help="also time one rank's share of the 70B-shaped workload under this tensor-parallel "
+                        "degree (attention with heads / N, argmax over vocabulary / N); 0 = skip")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="approximate CPU time budget of the oracle baseline sample")
@@ -260,34 +263,46 @@ def measured_traffic(workload: int, kernel: str):
     return total
 
 
-def attention_alone(n, calls=10):
+def attention_alone(n, calls=10, tp=1):
     """Tree attention alone, back to back, on workload `n` (its K/V exceed the
     MALL, so no call finds the previous one's data there): mean event-timed
-    duration per call and its roofline fractions."""
+    duration per call and its roofline fractions.  With tp > 1: one
+    tensor-parallel rank's share of the workload (heads and vocabulary / tp),
+    and its argmax over the local vocabulary columns timed the same way."""
     import numpy as np
     import torch
     from paper_2501_12162_amd.device import DeviceBatch
     from paper_2501_12162_amd.workload import WORKLOAD_NAMES, make_config
-    b = make_config(n)
+    b = make_config(n, tp=tp)
     costs = algorithmic_costs(b)
     d = DeviceBatch(b)
     stream = torch.cuda.current_stream()
-    for _ in range(3):
-        d.attention(stream)
-    torch.cuda.synchronize()
-    ev = [KernelTimer() for _ in range(calls + 1)]
-    ev[0].record(stream)
-    for i in range(calls):
-        d.attention(stream)
-        ev[i + 1].record(stream)
-    torch.cuda.synchronize()
-    us = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(calls)]) * 1e3
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ev = [KernelTimer() for _ in range(calls + 1)]
+        hold_gpu()
+        ev[0].record(stream)
+        for i in range(calls):
+            fn()
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        return np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(calls)]) * 1e3
+    us = timed(lambda: d.attention(stream))
     mean = float(us.mean())
-    return {"workload": WORKLOAD_NAMES[n], "tree_attn_us": mean, "tree_attn_p50_us": float(np.median(us)),
-            "mfma_frac": costs["attn_flops"] / (mean * 1e-6) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
-            "hbm_frac": costs["attn_bytes"] / (mean * 1e-6) / 1e9 / HBM_PEAK_GBS,
-            "alg_flops": costs["attn_flops"], "alg_bytes": costs["attn_bytes"],
-            "traffic": measured_traffic(n, "tree_attn"), "calls": calls}
+    res = {"workload": b.meta["workload"], "tree_attn_us": mean, "tree_attn_p50_us": float(np.median(us)),
+           "mfma_frac": costs["attn_flops"] / (mean * 1e-6) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
+           "hbm_frac": costs["attn_bytes"] / (mean * 1e-6) / 1e9 / HBM_PEAK_GBS,
+           "alg_flops": costs["attn_flops"], "alg_bytes": costs["attn_bytes"],
+           "traffic": measured_traffic(n, "tree_attn") if tp == 1 else None, "calls": calls}
+    if tp > 1:
+        am = timed(lambda: d.argmax(stream))
+        res.update({"tp": tp, "q_heads": b.num_q_heads, "kv_heads": b.num_kv_heads, "vocab_columns": b.vocab,
+                    "node_argmax_us": float(am.mean()),
+                    "node_argmax_hbm_frac": costs["argmax_bytes"] / (float(am.mean()) * 1e-6) / 1e9 / HBM_PEAK_GBS})
+    return res
 
 
 def _finite(x):
@@ -691,6 +706,9 @@ def main():
     }
     if extra is not None:
         line["mfma_bound_attention"] = extra
+    if args.tp_share > 1:
+        progress("one tensor-parallel rank's share of workload 4")
+        line["tp_rank_share"] = attention_alone(4, tp=args.tp_share)
     if not args.no_cpu_baseline:
         progress("oracle baseline on the host cores")
         line["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds)

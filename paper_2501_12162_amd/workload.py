@@ -352,8 +352,13 @@ NATURAL_TIE_RATE = 0.085
 SHORT_NAMES = {1: "tiny_f32", 2: "llama3_8b", 3: "mixed_slo", 4: "llama3_70b_shape", 5: "long_context"}
 
 
-def make_config(n: int, seed: Optional[int] = None) -> VerifyBatch:
-    """Draw the named workload ``n`` (1..5) with seed ``12162 + n``."""
+def make_config(n: int, seed: Optional[int] = None, tp: int = 1) -> VerifyBatch:
+    """Draw the named workload ``n`` (1..5) with seed ``12162 + n``.
+
+    ``tp`` > 1 draws one tensor-parallel rank's share of it instead: the
+    same trees and prefix lengths, 1/tp of the q- and kv-heads (whole head
+    groups) and the first ceil(V / tp) columns' worth of vocabulary (a
+    vocab-sharded LM head's local logits)."""
     if seed is None:
         seed = 12162 + n
     rng = np.random.Generator(np.random.PCG64(seed))
@@ -398,12 +403,19 @@ def make_config(n: int, seed: Optional[int] = None) -> VerifyBatch:
                   p_match=0.8, logit_std=2.0)
     else:
         raise ValueError("workloads are numbered 1..5")
+    if tp > 1:
+        if kw["num_kv_heads"] % tp:
+            raise ValueError("tp must divide the kv-head count")
+        kw["num_q_heads"] //= tp
+        kw["num_kv_heads"] //= tp
+        kw["vocab"] = -(-kw["vocab"] // tp)
     if kw["dtype"] == "bf16":
         kw["tie_rate"] = NATURAL_TIE_RATE
     b = make_batch(parents=parents, prefix_lens=lens, page_size=16, seed=seed,
                    name=SHORT_NAMES[n], rng=rng, **kw)
-    b.meta["workload"] = WORKLOAD_NAMES[n]
+    b.meta["workload"] = WORKLOAD_NAMES[n] + (" (one of %d tensor-parallel ranks)" % tp if tp > 1 else "")
     b.meta["config"] = n
+    b.meta["tp"] = tp
     return b
 
 

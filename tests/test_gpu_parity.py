@@ -75,6 +75,18 @@ def test_named_workload(torch_cuda, cfg):
         assert (b.planted_ties > 1).sum() >= 0.04 * b.total_nodes
 
 
+def test_tensor_parallel_rank_share(torch_cuda):
+    """One rank's share of the 70B-shaped workload under 4-way tensor
+    parallelism (16 q-heads, 2 kv-heads, a quarter of the vocabulary): every
+    node against the oracle."""
+    from paper_2501_12162_amd.workload import make_config
+    b = make_config(4, tp=4)
+    assert (b.num_q_heads, b.num_kv_heads, b.vocab) == (16, 2, 32064)
+    _, (out, amax, alen, tok, nodes) = run_device(b)
+    check_attention(b, out)
+    check_argmax_accept(b, amax, alen, tok, nodes)
+
+
 def _ragged_batch(dtype, head_dim, seed, hq=8, hkv=2):
     rng = np.random.Generator(np.random.PCG64(seed))
     sizes = [1, 5, 33, 64, 100, 128]
