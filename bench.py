@@ -33,13 +33,16 @@ FP32_PEAK_TFLOPS = 157.3
 METRIC = "verified tree tokens/sec + % peak HBM GB/s, tree-verify attention, 1 MI355X"
 MALL_BYTES = 256 << 20
 EVENT_EVERY = 5                 # the last 1/EVENT_EVERY of the timed steps carry per-kernel events
+WARM_MS = 30.0                  # continuous GPU work before any timed region (see warm())
 
 
 def parse_args():
     p = argparse.ArgumentParser(description=__doc__)
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=None,
+                   help="untimed warm-up steps (default: as many as keep the GPU busy for %d ms, at least 10)"
+                        % WARM_MS)
     p.add_argument("--workload", type=int, default=5, choices=[1, 2, 3, 4, 5],
                    help="1 tiny-f32, 2 llama3-8b, 3 mixed-slo, 4 70b-shape, 5 long-context (default)")
     p.add_argument("--unfused", action="store_true",
@@ -263,7 +266,7 @@ def measured_traffic(workload: int, kernel: str):
     return total
 
 
-def attention_alone(n, calls=10, tp=1):
+def attention_alone(n, calls=30, tp=1):
     """Tree attention alone, back to back, on workload `n` (its K/V exceed the
     MALL, so no call finds the previous one's data there): mean event-timed
     duration per call and its roofline fractions.  With tp > 1: one
@@ -279,9 +282,7 @@ def attention_alone(n, calls=10, tp=1):
     stream = torch.cuda.current_stream()
 
     def timed(fn):
-        for _ in range(3):
-            fn()
-        torch.cuda.synchronize()
+        warm(lambda k: d.attention(stream))
         ev = [KernelTimer() for _ in range(calls + 1)]
         hold_gpu()
         ev[0].record(stream)
@@ -314,6 +315,28 @@ def _finite(x):
     if isinstance(x, float) and not math.isfinite(x):
         return None
     return x
+
+
+def warm(fn, ms=WARM_MS, min_calls=10):
+    """Calls fn(0), fn(1), ... until the GPU has been kept busy for about
+    `ms` (and at least `min_calls` calls); returns the number of calls.
+
+    After any idle spell (the host drawing a workload, a synchronisation
+    followed by host work, a 100 ms pause) the GPU runs the same work slower
+    for its first ~10 ms: on the long-context batch the first ~40 one-call
+    steps take ~250 us each, later ones ~221 us, and 70B-shape attention
+    reads up to 20% slow, which is the behaviour of a clock that ramps up
+    under load.  Timed regions therefore follow this much work."""
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    k = 0
+    while k < min_calls or time.perf_counter() - t0 < ms * 1e-3:
+        for _ in range(4):
+            fn(k)
+            k += 1
+        torch.cuda.synchronize()
+    return k
 
 
 def hold_gpu(ms=3.0):
@@ -424,10 +447,13 @@ def main():
     calib_dst = torch.empty_like(calib_src)
     calib_dst.copy_(calib_src)
 
+    if args.warmup is None:
+        args.warmup = warm(run_step)
+    else:
+        for i in range(args.warmup):
+            run_step(i)
+        torch.cuda.synchronize()
     progress("timing %d steps after %d warm-up steps" % (args.steps, args.warmup))
-    for i in range(args.warmup):
-        run_step(i)
-    torch.cuda.synchronize()
 
     # Per-kernel HIP events (fence-free, see KernelTimer) on the last
     # 1/EVENT_EVERY of the timed steps only, so that the throughput is not
@@ -461,7 +487,7 @@ def main():
             k_tree=rp["k_tree"], v_tree=rp["v_tree"], k_pages=rp["k_pages"], v_pages=rp["v_pages"],
             block_table=dev.block_table, prefix_len=dev.prefix_len, new_prefix_len=new_len)
     commit()
-    torch.cuda.synchronize()
+    warm(run_step)   # back to the GPU's loaded clock after the host work above
     hold_gpu()   # the host enqueues every timed call before the GPU starts them
     commit_ev[0].record(stream)
     for _ in range(10):
@@ -489,7 +515,7 @@ def main():
                                   budget=cands.budget, n_max=cands.n_max, tree_size=s_size,
                                   tree_parent=s_par, tree_cand=s_cand)
     select()
-    torch.cuda.synchronize()
+    warm(run_step)
     hold_gpu()   # the host enqueues every timed call before the GPU starts them
     commit_ev[0].record(stream)
     for _ in range(10):
@@ -523,7 +549,7 @@ def main():
         ada.adaserve_beam_step(logits=beam_logits[i % beam_reps], vocab=b.vocab, beam_logprob=beam_lp,
                                out_parent=b_par, out_token=b_tok, out_logprob=b_lp, workspace=beam_ws)
     beam(0)
-    torch.cuda.synchronize()
+    warm(run_step)
     hold_gpu()   # the host enqueues every timed call before the GPU starts them
     commit_ev[0].record(stream)
     for i in range(20):
@@ -557,7 +583,7 @@ def main():
                                          u_accept=u_acc, u_bonus=u_bon, max_accept=dev.max_accept, accept_len=s_len,
                                          accept_tokens=s_tok, accept_nodes=s_nodes, workspace=s_ws)
     sampled()
-    torch.cuda.synchronize()
+    warm(run_step)
     hold_gpu()   # the host enqueues every timed call before the GPU starts them
     commit_ev[0].record(stream)
     for _ in range(10):
@@ -572,9 +598,9 @@ def main():
         # (each call's own events; the replicas keep the MALL cold)
         step_ms = np.array([e[0].elapsed_time(e[1]) for e in events.values()])
 
-        def alone(fn, calls=10):
+        def alone(fn, calls=30):
             ev = [KernelTimer() for _ in range(calls + 1)]
-            torch.cuda.synchronize()
+            warm(run_step)
             hold_gpu()   # the host enqueues every timed call before the GPU starts them
             ev[0].record(stream)
             for k in range(calls):
