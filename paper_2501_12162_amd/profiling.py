@@ -2,7 +2,7 @@
 
 Usage (on the GPU machine, after the runs named in each summary's header):
 
-  python -m paper_2501_12162_amd.profiling stats  <kernel_stats.csv> <out.md> "<command>"
+  python -m paper_2501_12162_amd.profiling stats  <kernel_stats.csv> <out.md> "<command>" [<kernel_trace.csv> <warmup> <steps>]
   python -m paper_2501_12162_amd.profiling traffic <fetch_dir> <write_dir> <workload> <out.json> "<commands>"
   python -m paper_2501_12162_amd.profiling counters <out.json> <workload> "<commands>" <dir> [<dir> ...]
 
@@ -90,6 +90,29 @@ def stats_markdown(csv_path: str, command: str) -> str:
             r["Name"][:90].replace("|", "/"), r["Calls"], float(r["AverageNs"]) / 1e3,
             float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
     return "\n".join(out) + "\n"
+
+
+def timed_step_summary(trace_csv: str, warmup: int, steps: int) -> dict:
+    """The verification launches of bench.py's timed loop, read from a
+    rocprofv3 kernel trace: the tree-attention dispatches number warmup ..
+    warmup + steps - 1 in dispatch order (one per step; the step's second
+    launch, the merge/acceptance kernel, is the dispatch after each).  Returns
+    the mean duration of each of the two launches over those steps and the
+    mean start-to-start interval of consecutive steps (the GPU's time per
+    step, gaps included)."""
+    rows = sorted(csv.DictReader(open(trace_csv)), key=lambda r: int(r["Dispatch_Id"]))
+    attn = [i for i, r in enumerate(rows) if kernel_kind(r["Kernel_Name"]) == "tree_attn"]
+    if len(attn) < warmup + steps:
+        raise RuntimeError("trace holds %d attention dispatches, fewer than %d" % (len(attn), warmup + steps))
+    idx = attn[warmup:warmup + steps]
+    dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    start = [int(rows[i]["Start_Timestamp"]) for i in idx]
+    res = {"steps": steps, "tree_attn_us": statistics.fmean(dur(rows[i]) for i in idx),
+           "start_to_start_us": (start[-1] - start[0]) / 1e3 / (steps - 1)}
+    nxt = [rows[i + 1] for i in idx if i + 1 < len(rows)]
+    if len(nxt) == steps and all(kernel_kind(r["Kernel_Name"]) == "tree_attn_combine" for r in nxt):
+        res["tree_attn_combine_us"] = statistics.fmean(dur(r) for r in nxt)
+    return res
 
 
 def _counter_rows(directory: str, counter: str):
@@ -194,6 +217,13 @@ def counter_summary(dirs, workload: int, commands: str, simds: int = 1024, xcds:
 def main(argv):
     if len(argv) >= 4 and argv[1] == "stats":
         md = stats_markdown(argv[2], argv[4] if len(argv) > 4 else "")
+        if len(argv) >= 8:
+            t = timed_step_summary(argv[5], int(argv[6]), int(argv[7]))
+            md += ("\nTimed loop only (dispatches %d to %d of the attention kernel, from the kernel trace): "
+                   "attention launch %.2f us" % (int(argv[6]), int(argv[6]) + t["steps"] - 1, t["tree_attn_us"]))
+            if "tree_attn_combine_us" in t:
+                md += ", second launch %.2f us" % t["tree_attn_combine_us"]
+            md += ", start to start %.2f us per step.\n" % t["start_to_start_us"]
         with open(argv[3], "w") as f:
             f.write(md)
         print(md)
