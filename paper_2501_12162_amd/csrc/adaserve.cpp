@@ -91,7 +91,7 @@ size_t adaserve_tree_attn_workspace_bytes(int32_t num_requests, const int32_t *n
   if (validate_attn_shape(num_requests, node_indptr_host, prefix_len_host, num_q_heads, num_kv_heads,
                           head_dim, page_size, dtype, -1, shape) != ADASERVE_OK)
     return SIZE_MAX;
-  return make_plan(num_requests, node_indptr_host, prefix_len_host, num_kv_heads, shape.group, head_dim, dtype)
+  return make_plan_cached(num_requests, node_indptr_host, prefix_len_host, num_kv_heads, shape.group, head_dim, dtype)
       .ws_bytes;
 }
 
@@ -172,7 +172,7 @@ int32_t tree_attn_verify_impl(int32_t num_requests, const int32_t *node_indptr, 
   for (const void *t : tensors)
     if (t && !aligned(t, 16)) return fail(ADASERVE_ERR_INVALID_ARGUMENT, "tensor pointers must be 16-byte aligned");
   const AttnPlan plan =
-      make_plan(num_requests, node_indptr_host, prefix_len_host, num_kv_heads, shape.group, head_dim, dtype);
+      make_plan_cached(num_requests, node_indptr_host, prefix_len_host, num_kv_heads, shape.group, head_dim, dtype);
   if (use_scratch) {
     if (plan.ws_bytes > (size_t)ADASERVE_TREE_ATTN_SCRATCH_BYTES)
       return fail(ADASERVE_ERR_WORKSPACE,

@@ -261,6 +261,34 @@ AttnPlan make_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_ho
   return best;
 }
 
+AttnPlan make_plan_cached(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
+                          int32_t group, int32_t head_dim, int32_t dtype) {
+  if (dtype != ADASERVE_BF16 || B <= 0) return make_plan(B, indptr_host, plen_host, hkv, group, head_dim, dtype);
+  struct Entry {
+    bool valid = false;
+    int32_t B = 0, hkv = 0, group = 0, head_dim = 0, dtype = 0;
+    std::vector<int32_t> indptr, plen;
+    AttnPlan plan;
+  };
+  thread_local Entry e;
+  const bool hit = e.valid && e.B == B && e.hkv == hkv && e.group == group && e.head_dim == head_dim &&
+                   e.dtype == dtype && std::equal(indptr_host, indptr_host + B + 1, e.indptr.begin()) &&
+                   std::equal(plen_host, plen_host + B, e.plen.begin());
+  if (!hit) {
+    e.valid = false;
+    e.plan = make_plan(B, indptr_host, plen_host, hkv, group, head_dim, dtype);
+    e.indptr.assign(indptr_host, indptr_host + B + 1);
+    e.plen.assign(plen_host, plen_host + B);
+    e.B = B;
+    e.hkv = hkv;
+    e.group = group;
+    e.head_dim = head_dim;
+    e.dtype = dtype;
+    e.valid = true;
+  }
+  return e.plan;
+}
+
 // Fills the dispatch-ordered request table (descending per-unit cost) when
 // the batch fits in the kernel arguments; otherwise leaves it empty.
 void fill_plan_table(PlanTable &t, int32_t B, const int32_t *indptr_host, const int32_t *plen_host,

@@ -57,6 +57,14 @@ double lpt_makespan(std::vector<std::pair<double, int64_t>> &units);
 AttnPlan make_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
                    int32_t group, int32_t head_dim, int32_t dtype);
 
+// make_plan through a one-entry cache per thread, keyed by the scalar
+// arguments and the contents of both host mirrors (not their addresses: a
+// caller may refill the same buffers between calls).  The workspace query
+// and the verify call of one batch then plan it once, and a batch verified
+// again (a retried or repeated step) costs a comparison of 2B + 1 integers.
+AttnPlan make_plan_cached(int32_t B, const int32_t *indptr_host, const int32_t *plen_host, int32_t hkv,
+                          int32_t group, int32_t head_dim, int32_t dtype);
+
 // The dispatch-ordered request table for batches of at most kPlanMax
 // requests (count = 0 otherwise).
 struct PlanTable {

@@ -139,6 +139,42 @@ static void check_plan(const Batch &b, int hq, int hkv, int D) {
   CHECK(prev_end == p.units && prev_g == t.merge_blocks, "table totals");
 }
 
+static bool same_plan(const AttnPlan &x, const AttnPlan &y) {
+  return x.rows_per_tile == y.rows_per_tile && x.chunk_target == y.chunk_target && x.chunk_floor == y.chunk_floor &&
+         x.chunk_len == y.chunk_len && x.units == y.units && x.padded_grid == y.padded_grid &&
+         x.row_groups == y.row_groups && x.needs_combine == y.needs_combine && x.ws_o_bytes == y.ws_o_bytes &&
+         x.ws_ml_bytes == y.ws_ml_bytes && x.ws_bytes == y.ws_bytes && x.est_us == y.est_us;
+}
+
+// The cached planner against a fresh plan on every call of a sequence that
+// repeats batches, refills the same buffers in place (one prefix grows by a
+// token, one tree loses a node) and changes only a scalar argument.
+static void check_plan_cache(std::mt19937_64 &rng) {
+  std::vector<int32_t> ip, pl;
+  for (int it = 0; it < 400; ++it) {
+    const int op = (int)(rng() % 5);
+    if (ip.empty() || op == 0) {
+      const Batch b = random_batch(rng, 1 + (int)(rng() % 40), 64, 20000);
+      ip = b.indptr;
+      pl = b.plen;
+    } else if (op == 1) {
+      pl[rng() % pl.size()] += 1;
+    } else if (op == 2) {
+      const size_t r = rng() % pl.size();
+      if (ip[r + 1] - ip[r] > 1)
+        for (size_t i = r + 1; i < ip.size(); ++i) ip[i] -= 1;
+    }  // op 3, 4: the same contents again
+    const int B = (int)pl.size();
+    const int hkv = op == 4 ? 2 : 8, G = op == 4 ? 16 : 4, D = it % 2 ? 128 : 64;
+    const AttnPlan fresh = make_plan(B, ip.data(), pl.data(), hkv, G, D, ADASERVE_BF16);
+    const AttnPlan cached = make_plan_cached(B, ip.data(), pl.data(), hkv, G, D, ADASERVE_BF16);
+    CHECK(same_plan(fresh, cached), "cached plan differs at step %d (op %d)", it, op);
+    CHECK(same_plan(fresh, make_plan_cached(B, ip.data(), pl.data(), hkv, G, D, ADASERVE_BF16)),
+          "second cached call differs at step %d", it);
+  }
+  CHECK(make_plan_cached(0, nullptr, nullptr, 8, 4, 128, ADASERVE_BF16).units == 0, "empty batch");
+}
+
 int main() {
   std::mt19937_64 rng(2501);
   // validation: malformed host mirrors and scalars give a status, never UB
@@ -182,6 +218,7 @@ int main() {
       check_plan(b, 32, 8, 128);
     }
   }
+  check_plan_cache(rng);
   // the makespan model against brute-force dealing
   for (int it = 0; it < 300; ++it) {
     std::vector<std::pair<double, int64_t>> u;
