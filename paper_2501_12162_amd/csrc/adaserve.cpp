@@ -219,6 +219,7 @@ int32_t tree_attn_verify_impl(int32_t num_requests, const int32_t *node_indptr, 
   a.padded_grid = plan.padded_grid;
   a.row_groups = plan.row_groups;
   a.merge_blocks = plan.row_groups * (kMaxRowsPerTile / 16);
+  a.stream_kv = plan.single_tile ? 1 : 0;
   if (dtype == ADASERVE_BF16) {
     PlanTable t;
     fill_plan_table(t, num_requests, node_indptr_host, prefix_len_host, num_kv_heads, shape.group, plan);

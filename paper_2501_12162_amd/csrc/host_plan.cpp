@@ -258,6 +258,9 @@ AttnPlan make_plan(int32_t B, const int32_t *indptr_host, const int32_t *plen_ho
       have = true;
     }
   }
+  best.single_tile = true;
+  for (int32_t r = 0; r < B; ++r)
+    best.single_tile &= row_tiles(indptr_host[r + 1] - indptr_host[r], group, rt) == 1;
   return best;
 }
 

@@ -40,6 +40,7 @@ struct AttnPlan {
   int64_t padded_grid = 0;
   int64_t row_groups = 0;
   bool needs_combine = false;
+  bool single_tile = false;        // every request fits one row tile: each K/V byte is read by one unit
   size_t ws_o_bytes = 0;
   size_t ws_ml_bytes = 0;
   size_t ws_bytes = 0;

@@ -52,6 +52,7 @@ struct TreeAttnArgs {
   int32_t *accept_len;         // [num_requests]
   int32_t *accept_tokens;      // [num_requests, max_accept]
   int32_t *accept_nodes;       // [num_requests, max_accept]
+  int32_t stream_kv;           // 1: every request is one row tile (K/V read once; non-temporal loads)
   int32_t plan_count;          // entries used in plan[] (0: scan the device arrays)
   PlanEntry plan[kPlanMax];
 };

@@ -93,6 +93,9 @@ static void check_plan(const Batch &b, int hq, int hkv, int D) {
   CHECK(units == p.units, "units %lld vs %lld", (long long)units, (long long)p.units);
   CHECK(groups == p.row_groups, "row groups");
   CHECK(split == p.needs_combine, "combine flag");
+  bool one_tile = true;
+  for (int r = 0; r < B; ++r) one_tile &= row_tiles(b.indptr[r + 1] - b.indptr[r], G, p.rows_per_tile) == 1;
+  CHECK(one_tile == p.single_tile, "single-tile flag");
   CHECK((p.ws_bytes == 0) == !split, "workspace %zu", p.ws_bytes);
   if (split) {
     CHECK(p.ws_o_bytes >= (size_t)p.units * kMaxRowsPerTile * D * 2, "partial outputs");
@@ -142,7 +145,8 @@ static void check_plan(const Batch &b, int hq, int hkv, int D) {
 static bool same_plan(const AttnPlan &x, const AttnPlan &y) {
   return x.rows_per_tile == y.rows_per_tile && x.chunk_target == y.chunk_target && x.chunk_floor == y.chunk_floor &&
          x.chunk_len == y.chunk_len && x.units == y.units && x.padded_grid == y.padded_grid &&
-         x.row_groups == y.row_groups && x.needs_combine == y.needs_combine && x.ws_o_bytes == y.ws_o_bytes &&
+         x.row_groups == y.row_groups && x.needs_combine == y.needs_combine && x.single_tile == y.single_tile &&
+         x.ws_o_bytes == y.ws_o_bytes &&
          x.ws_ml_bytes == y.ws_ml_bytes && x.ws_bytes == y.ws_bytes && x.est_us == y.est_us;
 }
 
