@@ -14,7 +14,9 @@ another instead, and ``--unfused --overlap`` runs the per-node argmax (which
 reads only the logits) on a second stream of the same priority beside the
 attention, joined before the acceptance.  Consecutive steps cycle through several
 copies of the inputs so that no step finds its K/V or logits in the 256 MB
-last-level (MALL) cache left behind by the previous one.
+last-level (MALL) cache left behind by the previous one.  Every timed
+region follows 30 ms of continuous GPU work (see warm()); by default the
+warm-up is as many steps as that takes, then 200 steps are timed.
 
 Prints ONE JSON line on stdout.
 """

@@ -13,7 +13,8 @@
 //    stages are in flight while one is multiplied, one barrier per block,
 //    waits counted by hand (vmcnt) so the ring really overlaps; steps that
 //    fetch whole prefix blocks run branch-free, five to a loop iteration,
-//    so their LDS addresses are constants;
+//    so their LDS addresses are constants; when every request is one row
+//    tile (no K/V byte is read twice) the loads carry the non-temporal hint;
 //  * LDS rows are XOR-swizzled in 16-byte chunks so that both the K
 //    fragment reads (16 keys x 16 B per quarter-wave) and the transposed V
 //    reads (ds_read_b64_tr_b16) hit distinct banks;
