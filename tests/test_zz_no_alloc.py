@@ -52,3 +52,52 @@ def test_noalloc_matches_the_workspace_entry_point():
         ref = oracle.tree_attn_batch(d.batch)
         err = float(np.abs(got - ref).max())
         assert err <= BF16_ABS and err <= BF16_REL * float(np.abs(ref).max()), err
+
+
+def _noalloc(ada, d, out, stream=None):
+    ada.adaserve_tree_attn_verify_noalloc(
+        node_indptr=d.node_indptr, node_indptr_host=d.node_indptr_host, parent=d.parent, q=d.q,
+        k_tree=d.k_tree, v_tree=d.v_tree, k_pages=d.k_pages, v_pages=d.v_pages,
+        block_table=d.block_table, prefix_len=d.prefix_len, prefix_len_host=d.prefix_len_host,
+        sm_scale=d.batch.sm_scale, out=out, stream=stream)
+
+
+def test_noalloc_replayed_from_a_graph():
+    """Captured in a HIP graph (what a caller that cannot allocate does) and
+    replayed three times, the output poisoned before each replay and an eager
+    allocation-free call on another batch between replays (it reuses the
+    same scratch): every replay and every eager call is bit-identical to the
+    workspace entry point on its batch."""
+    import torch
+    import paper_2501_12162_amd as ada
+    from paper_2501_12162_amd.device import DeviceBatch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    ada.load_library()
+    d = DeviceBatch(_batch(93, [32, 20, 32, 9], [12000, 5000, 9000, 3000]))
+    e = DeviceBatch(_batch(94, [7, 30], [2500, 6000]))
+    for x in (d, e):
+        assert 0 < x.workspace_bytes <= ada.TREE_ATTN_SCRATCH_BYTES
+        x.attention()
+    torch.cuda.synchronize()
+    ref_d, ref_e = d.out.clone(), e.out.clone()
+    out_d, out_e = torch.empty_like(d.out), torch.empty_like(e.out)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        _noalloc(ada, d, out_d, stream=side)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        _noalloc(ada, d, out_d, stream=torch.cuda.current_stream())
+    for rep in range(3):
+        print("graph replay", rep, flush=True)
+        out_d.fill_(float("nan"))
+        out_e.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out_d.view(torch.int16), ref_d.view(torch.int16)), rep
+        _noalloc(ada, e, out_e)
+        torch.cuda.synchronize()
+        assert torch.equal(out_e.view(torch.int16), ref_e.view(torch.int16)), rep
