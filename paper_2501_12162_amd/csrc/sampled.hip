@@ -32,6 +32,7 @@ namespace {
 
 constexpr int kThreads = 1024;
 constexpr int kStatsThreads = 256;
+constexpr int64_t kLastLevelCacheBytes = 256ll << 20;   // MI355X MALL (Infinity Cache)
 constexpr int kWaves = kThreads / 64;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kGroupVecs = 4 * kThreads;  // 16-byte vectors per pass iteration (four per thread)
@@ -300,7 +301,9 @@ __device__ int residual_draw(const char *prow, const char *qrow, int vocab, cons
 
 // Softmax statistics of every node's target and draft rows: one workgroup
 // per node, both rows in one pass.  stats[node] = (max_p, sum_p, max_q, sum_q).
-template <bool BF16>
+// NT: the rows are read with the non-temporal hint, for batches whose rows
+// do not fit the last-level cache anyway (see launch_sampled_accept).
+template <bool BF16, bool NT>
 __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArgs a) {
   constexpr int EPV = BF16 ? 8 : 4;
   constexpr int ESZ = BF16 ? 2 : 4;
@@ -320,8 +323,14 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
   const int nvec = a.vocab / EPV;
 #pragma unroll 4
   for (int i = t; i < nvec; i += kStatsThreads) {
-    const u32x4 w = *(const u32x4 *)(prow + (int64_t)i * 16);
-    const u32x4 z = *(const u32x4 *)(qrow + (int64_t)i * 16);
+    u32x4 w, z;
+    if constexpr (NT) {
+      w = __builtin_nontemporal_load((const u32x4 *)(prow + (int64_t)i * 16));
+      z = __builtin_nontemporal_load((const u32x4 *)(qrow + (int64_t)i * 16));
+    } else {
+      w = *(const u32x4 *)(prow + (int64_t)i * 16);
+      z = *(const u32x4 *)(qrow + (int64_t)i * 16);
+    }
     float wm = elem<BF16>(w, 0), zm = elem<BF16>(z, 0);
 #pragma unroll
     for (int e = 1; e < EPV; ++e) {
@@ -489,10 +498,20 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
 hipError_t launch_sampled_accept(const SampledArgs &a, bool bf16, hipStream_t stream) {
   if (a.num_requests == 0) return hipSuccess;
   if (a.total_nodes > 0) {
-    if (bf16)
-      hipLaunchKernelGGL(sampled_stats_kernel<true>, dim3((unsigned)a.total_nodes), dim3(kStatsThreads), 0, stream, a);
-    else
-      hipLaunchKernelGGL(sampled_stats_kernel<false>, dim3((unsigned)a.total_nodes), dim3(kStatsThreads), 0, stream, a);
+    // The walks read the rows of the nodes they visit again.  When both
+    // logits arrays fit the 256 MB MALL they are still there after the
+    // statistics pass (long-context batch, 131 MB: streaming the pass made
+    // the call 6% slower); larger batches stream it (4-8% faster measured).
+    const double row_bytes = 2.0 * (double)a.total_nodes * a.vocab * (bf16 ? 2 : 4);
+    const bool nt = row_bytes > (double)kLastLevelCacheBytes;
+    const dim3 grid((unsigned)a.total_nodes), block(kStatsThreads);
+    if (bf16) {
+      if (nt) hipLaunchKernelGGL((sampled_stats_kernel<true, true>), grid, block, 0, stream, a);
+      else hipLaunchKernelGGL((sampled_stats_kernel<true, false>), grid, block, 0, stream, a);
+    } else {
+      if (nt) hipLaunchKernelGGL((sampled_stats_kernel<false, true>), grid, block, 0, stream, a);
+      else hipLaunchKernelGGL((sampled_stats_kernel<false, false>), grid, block, 0, stream, a);
+    }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
