@@ -732,6 +732,14 @@ def main():
         "accepted_tokens_per_s": float(alen.sum()) * args.steps / wall,
         "device": dev_name,
     }
+    from paper_2501_12162_amd.workload import MODEL_LAYERS
+    layers = MODEL_LAYERS.get(args.workload)
+    if layers and math.isfinite(attn_us):
+        proj_us = layers * attn_us + argmax_us + accept_us
+        line["model_projection"] = {
+            "label": "projection, not a measurement: the attention call timed above repeated for every "
+                     "decoder layer, plus one argmax and one acceptance; the model's other layers left out",
+            "layers": layers, "step_us": proj_us, "tree_tokens_per_s": T / (proj_us * 1e-6)}
     if extra is not None:
         line["mfma_bound_attention"] = extra
     if args.tp_share > 1:

@@ -351,6 +351,11 @@ NATURAL_TIE_RATE = 0.085
 
 SHORT_NAMES = {1: "tiny_f32", 2: "llama3_8b", 3: "mixed_slo", 4: "llama3_70b_shape", 5: "long_context"}
 
+# Decoder layers of the model whose attention shape a workload takes
+# (Llama-3 8B: 32, Llama-3 70B: 80); only a labelled whole-model projection
+# uses them.
+MODEL_LAYERS = {2: 32, 3: 32, 4: 80, 5: 32}
+
 
 def make_config(n: int, seed: Optional[int] = None, tp: int = 1) -> VerifyBatch:
     """Draw the named workload ``n`` (1..5) with seed ``12162 + n``.
