@@ -623,6 +623,18 @@ def main():
         accept_ms = np.array([e[4].elapsed_time(e[5]) for e in events.values()])
         step_ms = np.array([e[0].elapsed_time(e[5]) for e in events.values()])
 
+    # Reference rate of the box: torch's device-to-device copy of 256 MiB
+    # (bytes read + written per second), timed after the steps so that the
+    # calibration copy stays the last copy before the first attention launch.
+    warm(lambda k: calib_dst.copy_(calib_src))
+    hold_gpu()
+    commit_ev[0].record(stream)
+    for _ in range(10):
+        calib_dst.copy_(calib_src)
+    commit_ev[1].record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 2 * calib_src.numel() * 10 / (commit_ev[0].elapsed_time(commit_ev[1]) * 1e-3) / 1e9
+
     # sanity: the last step's argmax must equal the planted maxima
     got = dev.target_argmax.cpu().numpy()
     if not np.array_equal(got, b.planted_argmax):
@@ -728,6 +740,8 @@ def main():
                                 ("step", step_ms))
             },
         },
+        "reference": {"device_copy_gbs": copy_gbs,
+                      "note": "torch device-to-device copy of 256 MiB, bytes read + written per second"},
         "accepted_tokens_per_step": int(alen.sum()),
         "accepted_tokens_per_s": float(alen.sum()) * args.steps / wall,
         "device": dev_name,
