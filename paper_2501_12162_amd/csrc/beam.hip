@@ -37,6 +37,8 @@
 // (unused slots) are not read at all.
 #include <limits.h>
 
+#include <type_traits>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -211,44 +213,60 @@ __global__ __launch_bounds__(64 * kScanWaves) void beam_scan_kernel(BeamArgs a) 
     const int n_valid = min(kChunk, a.vocab - first);
     const char *base = (const char *)a.logits + ((int64_t)row * a.row_stride + first) * ESZ;
     const uint32_t neg_inf_bits = BF16 ? 0xff80ff80u : 0xff800000u;
+    // Whole chunks (every chunk but a row's last) load in straight-line code
+    // and the pass follows in the same branch, so it starts on the first
+    // vector while the others are still in flight (where the loads sit under
+    // branches, or the two ways join before the pass, the compiler waits for
+    // all of them first).
     u32x4 w[kVecPerLane];
+    float vmax[kVecPerLane];
+    auto load_and_pass = [&](auto whole_chunk) {
+      if constexpr (decltype(whole_chunk)::value) {
 #pragma unroll
-    for (int v = 0; v < kVecPerLane; ++v) {
-      const int e0 = (v * 64 + lane) * EPV;
-      if (e0 + EPV <= n_valid) {
-        w[v] = __builtin_nontemporal_load((const u32x4 *)(base + (int64_t)e0 * ESZ));
+        for (int v = 0; v < kVecPerLane; ++v)
+          w[v] = __builtin_nontemporal_load((const u32x4 *)(base + (int64_t)(v * 64 + lane) * EPV * ESZ));
       } else {
-        u32x4 t = {neg_inf_bits, neg_inf_bits, neg_inf_bits, neg_inf_bits};
-        for (int e = 0; e < EPV && e0 + e < n_valid; ++e) {
-          if (BF16) {
-            const uint32_t h = ((const uint16_t *)base)[e0 + e];
-            t[e >> 1] = (e & 1) ? ((t[e >> 1] & 0xffffu) | (h << 16)) : ((t[e >> 1] & 0xffff0000u) | h);
+#pragma unroll
+        for (int v = 0; v < kVecPerLane; ++v) {
+          const int e0 = (v * 64 + lane) * EPV;
+          if (e0 + EPV <= n_valid) {
+            w[v] = __builtin_nontemporal_load((const u32x4 *)(base + (int64_t)e0 * ESZ));
           } else {
-            t[e] = ((const uint32_t *)base)[e0 + e];
+            u32x4 t = {neg_inf_bits, neg_inf_bits, neg_inf_bits, neg_inf_bits};
+            for (int e = 0; e < EPV && e0 + e < n_valid; ++e) {
+              if (BF16) {
+                const uint32_t h = ((const uint16_t *)base)[e0 + e];
+                t[e >> 1] = (e & 1) ? ((t[e >> 1] & 0xffffu) | (h << 16)) : ((t[e >> 1] & 0xffff0000u) | h);
+              } else {
+                t[e] = ((const uint32_t *)base)[e0 + e];
+              }
+            }
+            w[v] = t;
           }
         }
-        w[v] = t;
       }
-    }
-
-    // One pass: per-vector maxima, running lane maximum and sum.
-    float vmax[kVecPerLane];
+      // One pass: per-vector maxima, running lane maximum and sum.
 #pragma unroll
-    for (int v = 0; v < kVecPerLane; ++v) {
-      float m = elem<BF16>(w[v], 0);
+      for (int v = 0; v < kVecPerLane; ++v) {
+        float m = elem<BF16>(w[v], 0);
 #pragma unroll
-      for (int e = 1; e < EPV; ++e) m = fmaxf(m, elem<BF16>(w[v], e));
-      vmax[v] = m;
-      const float nm = fmaxf(lane_m, m);
-      if (nm > -INFINITY) {
-        const float off = -nm * kLog2e;
-        float add = 0.f;
+        for (int e = 1; e < EPV; ++e) m = fmaxf(m, elem<BF16>(w[v], e));
+        vmax[v] = m;
+        const float nm = fmaxf(lane_m, m);
+        if (nm > -INFINITY) {
+          const float off = -nm * kLog2e;
+          float add = 0.f;
 #pragma unroll
-        for (int e = 0; e < EPV; ++e) add += __builtin_amdgcn_exp2f(fmaf(elem<BF16>(w[v], e), kLog2e, off));
-        lane_s = fmaf(lane_s, __builtin_amdgcn_exp2f(fmaf(lane_m, kLog2e, off)), add);
-        lane_m = nm;
+          for (int e = 0; e < EPV; ++e) add += __builtin_amdgcn_exp2f(fmaf(elem<BF16>(w[v], e), kLog2e, off));
+          lane_s = fmaf(lane_s, __builtin_amdgcn_exp2f(fmaf(lane_m, kLog2e, off)), add);
+          lane_m = nm;
+        }
       }
-    }
+    };
+    if (n_valid == kChunk)
+      load_and_pass(std::true_type{});
+    else
+      load_and_pass(std::false_type{});
     // The widened values are recomputed below rather than kept live.
 #pragma unroll
     for (int v = 0; v < kVecPerLane; ++v) asm volatile("" : "+v"(w[v]));
