@@ -149,9 +149,10 @@ def test_fewer_children_than_slots(torch_cuda):
     check(torch_cuda, x, 3, lp, 8, "f32")
 
 
-def test_ties_dead_rows_and_neg_inf_logits(torch_cuda):
+@pytest.mark.parametrize("V", [3000, 16384])   # a ragged chunk only; whole chunks only (bf16 2, fp32 4)
+def test_ties_dead_rows_and_neg_inf_logits(torch_cuda, V):
     rng = np.random.Generator(np.random.PCG64(5))
-    V, B, w_in = 3000, 3, 4
+    B, w_in = 3, 4
     x = (rng.standard_normal((B * w_in, V)).astype(np.float32) * 2)
     x[0] = 0.0                                   # constant row: every token ties
     x[2] = x[1]                                  # identical rows, equal beam scores below
