@@ -78,18 +78,36 @@ __device__ float block_sum(float v, Shared &sh) {
   return t;
 }
 
-// The residual's unnormalised mass at token v: max(0, p(v) - c q(v)).
-// (Bulk sums use the hardware exp2, which flushes results below 2^-126 to
-// zero: such terms are far below the sums' rounding.)
+// A residual max(0, p(v) - c q(v)) (p itself when c = 0 or the node has no
+// child, hence no q), p = exp(x - mp) * ip and q = exp(y - mq) * iq.
 struct Residual {
-  float mp, ip, mq, iq, c;  // p = exp(x - mp) * ip, q = exp(y - mq) * iq
+  float mp, ip, mq, iq, c;
   bool has_q;
+};
+
+// Its unnormalised mass at token v, as the passes over a row evaluate it.
+// The normalisers and c go into the exponents, p = 2^(x log2 e + op) and
+// c q = 2^(y log2 e + oq), so a logit costs one FMA and one exp2 (a pass is
+// bound by one CU's ALU; the offsets are rounded once per pass, ~1e-6
+// relative to the terms).  Whether q enters (Q: the node has a child and
+// c != 0) is a template argument of the passes, so their loads are straight
+// -line code (a load under a branch makes the compiler wait for it before
+// the next).  (Bulk sums use the hardware exp2, which flushes results below
+// 2^-126 to zero: such terms are far below the sums' rounding.)
+template <bool Q>
+struct ResidualPass {
+  static constexpr bool kQ = Q;
+  float op, oq;
+  __device__ explicit ResidualPass(const Residual &R)
+      : op(-R.mp * kLog2e + log2f(R.ip)), oq(Q ? -R.mq * kLog2e + log2f(R.c * R.iq) : 0.f) {}
   __device__ __forceinline__ float at(float x, float y) const {
-    const float p = __builtin_amdgcn_exp2f((x - mp) * kLog2e) * ip;
-    if (!has_q || c == 0.f) return p;
-    return fmaxf(p - c * (__builtin_amdgcn_exp2f((y - mq) * kLog2e) * iq), 0.f);
+    const float p = __builtin_amdgcn_exp2f(fmaf(x, kLog2e, op));
+    if constexpr (!Q) return p;
+    return fmaxf(p - __builtin_amdgcn_exp2f(fmaf(y, kLog2e, oq)), 0.f);
   }
 };
+
+__device__ __forceinline__ bool q_enters(const Residual &R) { return R.has_q && R.c != 0.f; }
 
 // Round layout of a pass over a row: its 16-byte vectors go in groups of
 // kGroupVecs (in a group, thread t takes vectors t, t + kThreads, t +
@@ -107,8 +125,8 @@ struct Rounds {
 };
 
 // Sum over the vocabulary of the residual.
-template <bool BF16>
-__device__ float residual_mass(const char *prow, const char *qrow, int vocab, const Residual &R, Shared &sh) {
+template <bool BF16, class RT>
+__device__ float residual_mass_t(const char *prow, const char *qrow, int vocab, const RT &R, Shared &sh) {
   constexpr int EPV = BF16 ? 8 : 4;
   const int nvec = vocab / EPV;
   float s = 0.f;
@@ -119,7 +137,7 @@ __device__ float residual_mass(const char *prow, const char *qrow, int vocab, co
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       w[k] = *(const u32x4 *)(prow + (int64_t)(i + k * kThreads) * 16);
-      z[k] = R.has_q ? *(const u32x4 *)(qrow + (int64_t)(i + k * kThreads) * 16) : w[k];
+      z[k] = RT::kQ ? *(const u32x4 *)(qrow + (int64_t)(i + k * kThreads) * 16) : w[k];
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k)
@@ -128,21 +146,27 @@ __device__ float residual_mass(const char *prow, const char *qrow, int vocab, co
   }
   for (; i < nvec; i += kThreads) {
     const u32x4 w = *(const u32x4 *)(prow + (int64_t)i * 16);
-    const u32x4 z = R.has_q ? *(const u32x4 *)(qrow + (int64_t)i * 16) : w;
+    const u32x4 z = RT::kQ ? *(const u32x4 *)(qrow + (int64_t)i * 16) : w;
 #pragma unroll
     for (int e = 0; e < EPV; ++e) s += R.at(elem<BF16>(w, e), elem<BF16>(z, e));
   }
   for (int v = nvec * EPV + threadIdx.x; v < vocab; v += kThreads)
-    s += R.at(load_one<BF16>(prow, v), R.has_q ? load_one<BF16>(qrow, v) : 0.f);
+    s += R.at(load_one<BF16>(prow, v), RT::kQ ? load_one<BF16>(qrow, v) : 0.f);
   return block_sum(s, sh);
+}
+
+template <bool BF16>
+__device__ float residual_mass(const char *prow, const char *qrow, int vocab, const Residual &R, Shared &sh) {
+  if (q_enters(R)) return residual_mass_t<BF16>(prow, qrow, vocab, ResidualPass<true>(R), sh);
+  return residual_mass_t<BF16>(prow, qrow, vocab, ResidualPass<false>(R), sh);
 }
 
 // The residual's mass in each round (per wave in sh.rsum, then the
 // inclusive prefix over the rounds in sh.cum), for the bonus draw; returns
 // the total, the last prefix, so the two always agree.  (A rejection needs
 // only the total: residual_mass above, whose loop measured faster.)
-template <bool BF16>
-__device__ float residual_rounds(const char *prow, const char *qrow, int vocab, const Residual &R, Shared &sh) {
+template <bool BF16, class RT>
+__device__ float residual_rounds(const char *prow, const char *qrow, int vocab, const RT &R, Shared &sh) {
   constexpr int EPV = BF16 ? 8 : 4;
   const Rounds rd(vocab, EPV);
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -161,7 +185,7 @@ __device__ float residual_rounds(const char *prow, const char *qrow, int vocab, 
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       w[k] = *(const u32x4 *)(prow + (int64_t)(i0 + k * kThreads) * 16);
-      z[k] = R.has_q ? *(const u32x4 *)(qrow + (int64_t)(i0 + k * kThreads) * 16) : w[k];
+      z[k] = RT::kQ ? *(const u32x4 *)(qrow + (int64_t)(i0 + k * kThreads) * 16) : w[k];
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k)
@@ -172,12 +196,12 @@ __device__ float residual_rounds(const char *prow, const char *qrow, int vocab, 
   // the last, partial group (when there is one) and the tokens past the last vector
   for (int i = nfull * kGroupVecs + t; i < rd.nvec; i += kThreads) {
     const u32x4 w = *(const u32x4 *)(prow + (int64_t)i * 16);
-    const u32x4 z = R.has_q ? *(const u32x4 *)(qrow + (int64_t)i * 16) : w;
+    const u32x4 z = RT::kQ ? *(const u32x4 *)(qrow + (int64_t)i * 16) : w;
 #pragma unroll
     for (int e = 0; e < EPV; ++e) acc += R.at(elem<BF16>(w, e), elem<BF16>(z, e));
   }
   for (int v = rd.nvec * EPV + t; v < vocab; v += kThreads)
-    acc += R.at(load_one<BF16>(prow, v), R.has_q ? load_one<BF16>(qrow, v) : 0.f);
+    acc += R.at(load_one<BF16>(prow, v), RT::kQ ? load_one<BF16>(qrow, v) : 0.f);
   flush(rd.ngroups - 1);
   __syncthreads();
   if (wave == 0) {
@@ -202,9 +226,9 @@ __device__ float residual_rounds(const char *prow, const char *qrow, int vocab, 
 // One coalesced pass finds the round that holds the target; that round is
 // then read once more, each thread taking a contiguous run of its vectors so
 // that per-thread sums scan in token order.
-template <bool BF16>
-__device__ int residual_draw(const char *prow, const char *qrow, int vocab, const Residual &R, float u,
-                             Shared &sh) {
+template <bool BF16, class RT>
+__device__ int residual_draw_t(const char *prow, const char *qrow, int vocab, const RT &R, float u,
+                               Shared &sh) {
   constexpr int EPV = BF16 ? 8 : 4;
   residual_rounds<BF16>(prow, qrow, vocab, R, sh);
   const Rounds rd(vocab, EPV);
@@ -240,14 +264,17 @@ __device__ int residual_draw(const char *prow, const char *qrow, int vocab, cons
       for (int k = 0; k < 4; ++k) {
         const int64_t j = min(i + k, tv1 - 1);
         w[k] = *(const u32x4 *)(prow + j * 16);
-        z[k] = R.has_q ? *(const u32x4 *)(qrow + j * 16) : w[k];
+        z[k] = RT::kQ ? *(const u32x4 *)(qrow + j * 16) : w[k];
       }
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        if (i + k >= tv1) break;
+        // a slot past the run (its load repeats the run's last vector) adds
+        // exactly nothing and moves neither `last` nor `found`; masking it
+        // rather than leaving the loop keeps the loads above straight-line
+        const bool in_run = i + k < tv1;
 #pragma unroll
         for (int e = 0; e < EPV; ++e) {
-          const float r = R.at(elem<BF16>(w[k], e), elem<BF16>(z[k], e));
+          const float r = in_run ? R.at(elem<BF16>(w[k], e), elem<BF16>(z[k], e)) : 0.f;
           acc += r;
           const int v = (int)((i + k) * EPV) + e;
           if (r > 0.f) last = v;
@@ -257,7 +284,7 @@ __device__ int residual_draw(const char *prow, const char *qrow, int vocab, cons
     }
     if (tail)
       for (int v = rd.nvec * EPV; v < vocab; ++v) {
-        const float r = R.at(load_one<BF16>(prow, v), R.has_q ? load_one<BF16>(qrow, v) : 0.f);
+        const float r = R.at(load_one<BF16>(prow, v), RT::kQ ? load_one<BF16>(qrow, v) : 0.f);
         acc += r;
         if (r > 0.f) last = v;
         if (stop && found < 0 && acc > goal) found = v;
@@ -297,6 +324,13 @@ __device__ int residual_draw(const char *prow, const char *qrow, int vocab, cons
     __syncthreads();
   }
   return pick;
+}
+
+template <bool BF16>
+__device__ int residual_draw(const char *prow, const char *qrow, int vocab, const Residual &R, float u,
+                             Shared &sh) {
+  if (q_enters(R)) return residual_draw_t<BF16>(prow, qrow, vocab, ResidualPass<true>(R), u, sh);
+  return residual_draw_t<BF16>(prow, qrow, vocab, ResidualPass<false>(R), u, sh);
 }
 
 // Softmax statistics of every node's target and draft rows: one workgroup
