@@ -355,16 +355,12 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
     }
   };
   const int nvec = a.vocab / EPV;
-#pragma unroll 4
-  for (int i = t; i < nvec; i += kStatsThreads) {
-    u32x4 w, z;
-    if constexpr (NT) {
-      w = __builtin_nontemporal_load((const u32x4 *)(prow + (int64_t)i * 16));
-      z = __builtin_nontemporal_load((const u32x4 *)(qrow + (int64_t)i * 16));
-    } else {
-      w = *(const u32x4 *)(prow + (int64_t)i * 16);
-      z = *(const u32x4 *)(qrow + (int64_t)i * 16);
-    }
+  auto load = [&](const char *row, int i) -> u32x4 {
+    if constexpr (NT) return __builtin_nontemporal_load((const u32x4 *)(row + (int64_t)i * 16));
+    return *(const u32x4 *)(row + (int64_t)i * 16);
+  };
+  // one vector of each row into the running (max, sum) pairs
+  auto take = [&](const u32x4 &w, const u32x4 &z) {
     float wm = elem<BF16>(w, 0), zm = elem<BF16>(z, 0);
 #pragma unroll
     for (int e = 1; e < EPV; ++e) {
@@ -386,7 +382,22 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
       sq = (mq > -INFINITY ? sq * __builtin_amdgcn_exp2f((mq - nmq) * kLog2e) : 0.f) + acc;
       mq = nmq;
     }
+  };
+  // Four vectors of each row in flight per thread: all eight loads are
+  // written before the first use (the branches of `take` end the
+  // scheduler's regions, so it cannot hoist later loads above them).
+  int i = t;
+  for (; i + 3 * kStatsThreads < nvec; i += 4 * kStatsThreads) {
+    u32x4 w[4], z[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      w[k] = load(prow, i + k * kStatsThreads);
+      z[k] = load(qrow, i + k * kStatsThreads);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) take(w[k], z[k]);
   }
+  for (; i < nvec; i += kStatsThreads) take(load(prow, i), load(qrow, i));
   for (int v = nvec * EPV + t; v < a.vocab; v += kStatsThreads) {
     add(mp, sp, load_one<BF16>(prow, v));
     add(mq, sq, load_one<BF16>(qrow, v));
