@@ -75,7 +75,21 @@ __device__ __forceinline__ void argmax_row(const void *logits, int64_t row_strid
     for (int u = 0; u < kArgmaxUnroll; ++u)
       argmax_scan_vector<BF16>(w[u], head + (i + u * kThreads) * EPV, best, bi);
   }
-  for (; i < nvec; i += kThreads) argmax_scan_vector<BF16>(vp[i], head + i * EPV, best, bi);
+  if (i < nvec) {
+    // The last, partial batch: its loads still all go out together (one by
+    // one they were waited for in turn); slots past the end reload the last
+    // vector and are taken as -inf, which never replaces a lane's best.
+    constexpr uint32_t kNegInf = BF16 ? 0xff80ff80u : 0xff800000u;
+    u32x4 w[kArgmaxUnroll];
+#pragma unroll
+    for (int u = 0; u < kArgmaxUnroll; ++u) w[u] = __builtin_nontemporal_load(vp + min(i + u * kThreads, nvec - 1));
+#pragma unroll
+    for (int u = 0; u < kArgmaxUnroll; ++u) {
+      const bool in = i + u * kThreads < nvec;
+      argmax_scan_vector<BF16>(in ? w[u] : u32x4{kNegInf, kNegInf, kNegInf, kNegInf},
+                               head + (in ? i + u * kThreads : 0) * EPV, best, bi);
+    }
+  }
   for (int j = head + nvec * EPV + tid; j < vocab; j += kThreads)
     argmax_take_if_greater(argmax_load_scalar<BF16>(p, j), j, best, bi);
 

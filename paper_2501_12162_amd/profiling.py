@@ -28,7 +28,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CALIB_BYTES = 256 << 20
 
 
-_TRAFFIC_FILES = ("tree_attn.hip", "argmax.hip", "plan.h", "device_common.h", "host_plan.h", "host_plan.cpp")
+_TRAFFIC_FILES = ("tree_attn.hip", "argmax.hip", "argmax_row.h", "accept_wave.h", "plan.h", "device_common.h",
+                  "host_plan.h", "host_plan.cpp")
 
 
 def _block(text: str, start: str, end: str) -> str:
