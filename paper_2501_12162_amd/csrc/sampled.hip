@@ -56,6 +56,8 @@ struct Shared {
   int32_t depth[kMaxSampledNodes];
   int32_t path[kMaxSampledNodes];
   int32_t out[kMaxSampledNodes];
+  int32_t first_child[kMaxSampledNodes];  // n when the node has none
+  int32_t last_child[kMaxSampledNodes];   // -1 when the node has none
   float red_a[kWaves];
   float red_b[kWaves];
   float scan[kThreads];
@@ -480,17 +482,26 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
     return;
   }
 
+  // every node's first and last child (children follow their parent, and the
+  // walk takes a node's children in index order), found once for the walk
+  for (int i = t; i < n; i += kThreads) {
+    sh.first_child[i] = n;
+    sh.last_child[i] = -1;
+  }
+  __syncthreads();
+  for (int i = t + 1; i < n; i += kThreads) {  // parent[i] in [0, i): checked above
+    atomicMin(&sh.first_child[sh.parent[i]], i);
+    atomicMax(&sh.last_child[sh.parent[i]], i);
+  }
+  __syncthreads();
+
   int u = 0, len = 1;  // current node, path length
   if (t == 0) sh.path[0] = 0;
   while (true) {
     const char *prow = (const char *)a.target_logits + ((int64_t)(base + u) * a.row_stride) * ESZ;
     const char *qrow = (const char *)a.draft_logits + ((int64_t)(base + u) * a.row_stride) * ESZ;
-    int first_child = -1;
-    for (int i = u + 1; i < n; ++i)
-      if (sh.parent[i] == u) {
-        first_child = i;
-        break;
-      }
+    const int first_child = sh.first_child[u] < n ? sh.first_child[u] : -1;
+    const int last_child = sh.last_child[u];
     const float4 st = a.stats[base + u];
     Residual R;
     R.mp = st.x;
@@ -501,6 +512,8 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
     R.c = 0.f;
     float S = 1.f;  // mass of the current residual (exactly 1 for p itself)
     int next = -1;
+    bool after_last = false;  // the last child was rejected: draw from its residual R2
+    Residual R2 = R;
     for (int c = first_child; c >= 0 && c < n; ++c) {
       if (sh.parent[c] != u) continue;
       const int tok = sh.token[c];
@@ -511,15 +524,27 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
         next = c;
         break;
       }
-      Residual R2 = R;
+      R2 = R;
       R2.c = R.c + S;
+      // After the last child no acceptance test needs the new mass: the
+      // draw's own pass sums the same residual (no separate pass here)
+      if (c == last_child) {
+        after_last = true;
+        break;
+      }
       const float S2 = residual_mass<BF16>(prow, qrow, a.vocab, R2, sh);
       if (!(S2 > 0.f)) break;  // no mass left (rounding): draw from the residual before it
       R = R2;
       S = S2;
     }
     if (next < 0) {
-      const int v = residual_draw<BF16>(prow, qrow, a.vocab, R, a.u_bonus[base + u], sh);
+      // After the last child, draw from R2; -1 means that rejection left no
+      // mass (a sum of non-negative terms is zero only when every term is),
+      // and the draw is taken from the residual before it (one call site,
+      // so the draw's code is not inlined twice)
+      int v = -1;
+      for (int attempt = after_last ? 0 : 1; attempt < 2 && v < 0; ++attempt)
+        v = residual_draw<BF16>(prow, qrow, a.vocab, attempt == 0 ? R2 : R, a.u_bonus[base + u], sh);
       if (t == 0) sh.out[len - 1] = v;
       break;
     }
