@@ -231,3 +231,39 @@ def test_malformed_requests(torch_cuda):
     got = _run(torch_cuda, indptr, parent, draft, tl, dl, V, make_uniforms(rng, 13), make_uniforms(rng, 13), 2)
     assert got[0][:4].tolist() == [-1, -1, -1, -1] and got[0][4] == 1
     assert (got[1][:4] == -1).all() and (got[2][:4] == -1).all()
+
+
+def test_rejection_that_leaves_no_mass(torch_cuda):
+    """Target and draft one-hot at the same token A, every child proposing
+    another token: each child is rejected (its q is 0), and the rejection
+    leaves no mass (p - q = 0 everywhere), so the bonus is drawn from p
+    itself: A, with nothing accepted.  Roots with one child take the path
+    where the rejected child is the last one; roots with 2-4 children take
+    it after a pass that finds no mass.  Decided exactly on both sides (all
+    probabilities are 0 or 1), so every request must match."""
+    rng = np.random.Generator(np.random.PCG64(12))
+    V, B = 3000, 8
+    parents = [np.array([-1] + [0] * k, np.int32) for k in (1, 2, 3, 4, 1, 2, 3, 4)]
+    indptr = np.cumsum([0] + [p.size for p in parents]).astype(np.int32)
+    parent = np.concatenate(parents)
+    T = int(indptr[-1])
+    hot = rng.integers(0, V, size=T)
+    tl = np.full((T, V), -np.inf, np.float32)
+    tl[np.arange(T), hot] = 0.0
+    dl = tl.copy()
+    draft = np.zeros(T, np.int32)
+    for r in range(B):
+        a = hot[indptr[r]]
+        for i in range(indptr[r] + 1, indptr[r + 1]):
+            draft[i] = (a + 1 + rng.integers(0, V - 1)) % V   # never the root's hot token
+    ua, ub = make_uniforms(rng, T), make_uniforms(rng, T)
+    alen, tok, nodes = _run(torch_cuda, indptr, parent, draft, tl, dl, V, ua, ub, 6)
+    ref = oracle.tree_accept_sampled(node_indptr=indptr, parent=parent, draft_tokens=draft,
+                                     target_logits=tl.astype(np.float64), draft_logits=dl.astype(np.float64),
+                                     vocab=V, u_accept=np.asarray(ua, np.float32).astype(np.float64),
+                                     u_bonus=np.asarray(ub, np.float32).astype(np.float64), max_accept=6)
+    for r in range(B):
+        a = int(hot[indptr[r]])
+        assert alen[r] == 1 and tok[r][0] == a and nodes[r][0] == 0, (r, alen[r], tok[r], a)
+        assert (tok[r][1:] == -1).all() and (nodes[r][1:] == -1).all()
+        assert ref[0][r] == 1 and ref[1][r][0] == a
