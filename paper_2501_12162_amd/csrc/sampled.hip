@@ -53,11 +53,9 @@ __device__ __forceinline__ float load_one(const void *row, int v) {
 struct Shared {
   int32_t parent[kMaxSampledNodes];
   int32_t token[kMaxSampledNodes];
-  int32_t depth[kMaxSampledNodes];
   int32_t path[kMaxSampledNodes];
   int32_t out[kMaxSampledNodes];
-  int32_t first_child[kMaxSampledNodes];  // n when the node has none
-  int32_t last_child[kMaxSampledNodes];   // -1 when the node has none
+  uint32_t kids[kMaxSampledNodes][kMaxSampledNodes / 32];  // bit c: node c is a child
   float red_a[kWaves];
   float red_b[kWaves];
   float scan[kThreads];
@@ -462,15 +460,20 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
     }
   }
   __syncthreads();
-  if (!sh.bad && t == 0) {
-    // depth of every node (parents come first), bounded by the output rows
-    int deepest = 0;
-    sh.depth[0] = 0;
-    for (int i = 1; i < n; ++i) {
-      sh.depth[i] = sh.depth[sh.parent[i]] + 1;
-      deepest = max(deepest, sh.depth[i]);
+  if (!sh.bad) {
+    // every node's depth must be below the output rows (K): each thread
+    // follows its nodes' parent chains, at most K steps (parents come first,
+    // checked above, so every chain reaches the root)
+    bool deep = false;
+    for (int i = t; i < n; i += kThreads) {
+      int v = i, d = 0;
+      while (v != 0 && d < K) {
+        v = sh.parent[v];
+        ++d;
+      }
+      deep |= d >= K;
     }
-    if (deepest > K - 1) sh.bad = 1;
+    if (deep) atomicOr(&sh.bad, 1);
   }
   __syncthreads();
   if (sh.bad) {
@@ -482,17 +485,12 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
     return;
   }
 
-  // every node's first and last child (children follow their parent, and the
-  // walk takes a node's children in index order), found once for the walk
-  for (int i = t; i < n; i += kThreads) {
-    sh.first_child[i] = n;
-    sh.last_child[i] = -1;
-  }
+  // every node's children as a bit set, built once for the walk (which
+  // takes a node's children in index order: lowest set bit first)
+  for (int i = t; i < n * (kMaxSampledNodes / 32); i += kThreads) sh.kids[i / (kMaxSampledNodes / 32)][i % (kMaxSampledNodes / 32)] = 0u;
   __syncthreads();
-  for (int i = t + 1; i < n; i += kThreads) {  // parent[i] in [0, i): checked above
-    atomicMin(&sh.first_child[sh.parent[i]], i);
-    atomicMax(&sh.last_child[sh.parent[i]], i);
-  }
+  for (int i = t + 1; i < n; i += kThreads)  // parent[i] in [0, i): checked above
+    atomicOr(&sh.kids[sh.parent[i]][i >> 5], 1u << (i & 31));
   __syncthreads();
 
   int u = 0, len = 1;  // current node, path length
@@ -500,8 +498,24 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
   while (true) {
     const char *prow = (const char *)a.target_logits + ((int64_t)(base + u) * a.row_stride) * ESZ;
     const char *qrow = (const char *)a.draft_logits + ((int64_t)(base + u) * a.row_stride) * ESZ;
-    const int first_child = sh.first_child[u] < n ? sh.first_child[u] : -1;
-    const int last_child = sh.last_child[u];
+    uint32_t kids[kMaxSampledNodes / 32];
+#pragma unroll
+    for (int w = 0; w < kMaxSampledNodes / 32; ++w) kids[w] = __builtin_amdgcn_readfirstlane(sh.kids[u][w]);
+    // the lowest child above c (-1: none), the first child, the last child
+    auto next_kid = [&](int c) {
+#pragma unroll
+      for (int w = 0; w < kMaxSampledNodes / 32; ++w) {
+        const int lo = c + 1 - 32 * w;  // first eligible bit of word w
+        const uint32_t m = lo <= 0 ? kids[w] : lo >= 32 ? 0u : kids[w] & ~((1u << lo) - 1u);
+        if (m) return 32 * w + __builtin_ctz(m);
+      }
+      return -1;
+    };
+    const int first_child = next_kid(-1);
+    int last_child = -1;
+#pragma unroll
+    for (int w = 0; w < kMaxSampledNodes / 32; ++w)
+      if (kids[w]) last_child = 32 * w + 31 - __builtin_clz(kids[w]);
     const float4 st = a.stats[base + u];
     Residual R;
     R.mp = st.x;
@@ -514,8 +528,7 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
     int next = -1;
     bool after_last = false;  // the last child was rejected: draw from its residual R2
     Residual R2 = R;
-    for (int c = first_child; c >= 0 && c < n; ++c) {
-      if (sh.parent[c] != u) continue;
+    for (int c = first_child; c >= 0; c = next_kid(c)) {
       const int tok = sh.token[c];
       const float pt = exp2f((load_one<BF16>(prow, tok) - R.mp) * kLog2e) * R.ip;
       const float qt = exp2f((load_one<BF16>(qrow, tok) - R.mq) * kLog2e) * R.iq;

@@ -267,3 +267,27 @@ def test_rejection_that_leaves_no_mass(torch_cuda):
         assert alen[r] == 1 and tok[r][0] == a and nodes[r][0] == 0, (r, alen[r], tok[r], a)
         assert (tok[r][1:] == -1).all() and (nodes[r][1:] == -1).all()
         assert ref[0][r] == 1 and ref[1][r][0] == a
+
+
+def test_depth_limit_boundary(torch_cuda):
+    """Chains of six nodes (depth 5): walked with six output rows, refused
+    (-1) with five; the same on the oracle."""
+    rng = np.random.Generator(np.random.PCG64(13))
+    V = 512
+    parents = [chain_tree(6)] * 4
+    indptr = np.cumsum([0] + [p.size for p in parents]).astype(np.int32)
+    parent = np.concatenate(parents)
+    T = int(indptr[-1])
+    tl = (rng.standard_normal((T, V)) * 3).astype(np.float32)
+    dl = make_draft_logits(rng, tl, V, "f32", 0.2)
+    draft = rng.integers(0, V, size=T).astype(np.int32)
+    ua, ub = make_uniforms(rng, T), make_uniforms(rng, T)
+    for K, ok in ((6, True), (5, False)):
+        alen, tok, nodes = _run(torch_cuda, indptr, parent, draft, tl, dl, V, ua, ub, K)
+        ref = oracle.tree_accept_sampled(node_indptr=indptr, parent=parent, draft_tokens=draft,
+                                         target_logits=tl.astype(np.float64), draft_logits=dl.astype(np.float64),
+                                         vocab=V, u_accept=np.asarray(ua, np.float32).astype(np.float64),
+                                         u_bonus=np.asarray(ub, np.float32).astype(np.float64), max_accept=K)
+        assert ((alen >= 1) == ok).all() and ((ref[0] >= 1) == ok).all(), (K, alen, ref[0])
+        if not ok:
+            assert (tok == -1).all() and (nodes == -1).all()
