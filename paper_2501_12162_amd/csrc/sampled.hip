@@ -17,7 +17,8 @@
 // node's softmax statistics (max and exp-sum of its target and draft rows)
 // across the whole chip; the walk -- one workgroup of 1024 threads per
 // request -- then reads them, so an acceptance test costs two logits, a
-// rejection one pass over the node's two rows (the new S), and the bonus
+// rejection one pass over the node's two rows (the new S; none after the
+// node's last child, whose residual the draw sums anyway), and the bonus
 // draw one pass that sums the residual over at most 64 consecutive token
 // ranges ("rounds"), then a second over the one round that holds its
 // target.
