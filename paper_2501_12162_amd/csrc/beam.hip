@@ -179,6 +179,7 @@ __device__ __forceinline__ void rank_into(const uint64_t *cand, int n, int K, ui
   const int lane = threadIdx.x & 63;
   const uint64_t c = lane < n ? cand[lane] : 0;
   int rank = 0;
+#pragma unroll 8
   for (int j = 0; j < n; ++j) rank += cand[j] > c;
   if (lane < n && rank < K) out[rank] = c;
   if (lane >= n && lane < K) out[lane] = 0;
@@ -392,6 +393,7 @@ __global__ __launch_bounds__(64 * kScanWaves) void beam_scan_kernel(BeamArgs a) 
   if (t < n) {
     const uint64_t c = lst[t];
     int rank = 0, nz = 0;
+#pragma unroll 8
     for (int j = 0; j < n; ++j) {
       const uint64_t e = lst[j];
       rank += e > c;
@@ -458,6 +460,7 @@ __global__ __launch_bounds__(kMergeThreads) void beam_merge_kernel(BeamArgs a) {
       const int base = c / per_beam * per_beam;
       const uint64_t key = cand[c];
       int rank = 0, nz = 0;
+#pragma unroll 8
       for (int j = 0; j < per_beam; ++j) {
         const uint64_t e = cand[base + j];
         rank += e > key;
@@ -471,7 +474,34 @@ __global__ __launch_bounds__(kMergeThreads) void beam_merge_kernel(BeamArgs a) {
     __syncthreads();
   }
 
-  // Head merge across the beams' sorted lists: lane b follows beam b.
+  // The beam_out best of the W·K listed children.  When every one of them
+  // has a thread, each is placed by counting the larger keys (keys are
+  // unique; 0 = no child); otherwise a head merge across the beams' sorted
+  // lists, lane b following beam b, takes the best head beam_out times.
+  if (W * K <= kMergeThreads) {
+    const int all = W * K;
+    const uint64_t c = t < all ? blist[t] : 0;
+    int rank = 0, nz = 0;
+    if (t < all) {
+#pragma unroll 8
+      for (int j = 0; j < all; ++j) {
+        const uint64_t e = blist[j];
+        rank += e > c;
+        nz += e != 0;
+      }
+    }
+    if (c != 0 && rank < K) {
+      a.out_parent[r * K + rank] = 63 - (int)((c >> 20) & 63);
+      a.out_token[r * K + rank] = 0xfffff - (int)(c & 0xfffff);
+      a.out_logprob[r * K + rank] = key_value((uint32_t)(c >> 32));
+    }
+    if (t < K && t >= nz) {  // fewer children than slots (t < K <= all, so nz is this thread's count)
+      a.out_parent[r * K + t] = -1;
+      a.out_token[r * K + t] = -1;
+      a.out_logprob[r * K + t] = -INFINITY;
+    }
+    return;
+  }
   if (t >= 64) return;
   int head = 0;
   uint64_t cur = lane < W ? blist[lane * K] : 0;
