@@ -27,7 +27,8 @@
 //    sum) into lse per beam, adds log f(b) - lse to the parts' listed
 //    logits (the offset is the same for a whole row, so a row's best
 //    children by logit are its best by score), ranks each beam's candidates
-//    by counting, and merges the beams' sorted lists head by head in
+//    by counting, and takes the beam_out best of the beams' lists: each
+//    placed by counting when they all have a thread, else head by head in
 //    beam_out rounds of a wave maximum.
 //
 // Entries travel as 64-bit keys whose unsigned order is the ranking order
