@@ -262,3 +262,13 @@ def test_chained_steps_replayed_from_a_graph(torch_cuda):
                 assert torch.equal(a_, b_), (rep, k)
         chain()   # eager work between replays
         torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("w_in,w_out", [(16, 16), (17, 16), (4, 64)])
+def test_final_selection_both_forms(torch_cuda, w_in, w_out):
+    """W·K = 256 and 4·64 = 256 place the children by rank (one thread
+    each); 17·16 = 272 takes the head merge: both give the oracle's
+    children in its order."""
+    rng = np.random.Generator(np.random.PCG64(w_in * 100 + w_out))
+    b = make_beam_batch(rng, 3, w_in, 5000)
+    check(torch_cuda, b.logits, b.vocab, b.beam_logprob, w_out, "bf16")
