@@ -57,6 +57,12 @@ struct Shared {
   int32_t path[kMaxSampledNodes];
   int32_t out[kMaxSampledNodes];
   uint32_t kids[kMaxSampledNodes][kMaxSampledNodes / 32];  // bit c: node c is a child
+  // for each child c of the node being tested: the two logits of c's token
+  // at the node, c's acceptance uniform and c's own softmax statistics
+  float kid_p[kMaxSampledNodes];
+  float kid_q[kMaxSampledNodes];
+  float kid_u[kMaxSampledNodes];
+  float4 kid_st[kMaxSampledNodes];
   float red_a[kWaves];
   float red_b[kWaves];
   float scan[kThreads];
@@ -517,7 +523,18 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
 #pragma unroll
     for (int w = 0; w < kMaxSampledNodes / 32; ++w)
       if (kids[w]) last_child = 32 * w + 31 - __builtin_clz(kids[w]);
-    const float4 st = a.stats[base + u];
+    // One round of loads for every child's test inputs (thread c takes
+    // child c); the tests themselves run in order below.  The accepted
+    // child's statistics are then already here when it becomes the node.
+    if (t < n && ((sh.kids[u][t >> 5] >> (t & 31)) & 1u)) {
+      const int tk = sh.token[t];
+      sh.kid_p[t] = load_one<BF16>(prow, tk);
+      sh.kid_q[t] = load_one<BF16>(qrow, tk);
+      sh.kid_u[t] = a.u_accept[base + t];
+      sh.kid_st[t] = a.stats[base + t];
+    }
+    const float4 st = u == 0 ? a.stats[base] : sh.kid_st[u];
+    __syncthreads();
     Residual R;
     R.mp = st.x;
     R.ip = 1.f / st.y;
@@ -530,11 +547,10 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
     bool after_last = false;  // the last child was rejected: draw from its residual R2
     Residual R2 = R;
     for (int c = first_child; c >= 0; c = next_kid(c)) {
-      const int tok = sh.token[c];
-      const float pt = exp2f((load_one<BF16>(prow, tok) - R.mp) * kLog2e) * R.ip;
-      const float qt = exp2f((load_one<BF16>(qrow, tok) - R.mq) * kLog2e) * R.iq;
+      const float pt = exp2f((sh.kid_p[c] - R.mp) * kLog2e) * R.ip;
+      const float qt = exp2f((sh.kid_q[c] - R.mq) * kLog2e) * R.iq;
       const float rt = (R.c == 0.f ? pt : fmaxf(pt - R.c * qt, 0.f)) / S;
-      if (a.u_accept[base + c] * qt < rt) {
+      if (sh.kid_u[c] * qt < rt) {
         next = c;
         break;
       }
