@@ -494,7 +494,10 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
 
   // every node's children as a bit set, built once for the walk (which
   // takes a node's children in index order: lowest set bit first)
-  for (int i = t; i < n * (kMaxSampledNodes / 32); i += kThreads) sh.kids[i / (kMaxSampledNodes / 32)][i % (kMaxSampledNodes / 32)] = 0u;
+  {
+    uint32_t *words = &sh.kids[0][0];
+    for (int i = t; i < n * (kMaxSampledNodes / 32); i += kThreads) words[i] = 0u;
+  }
   __syncthreads();
   for (int i = t + 1; i < n; i += kThreads)  // parent[i] in [0, i): checked above
     atomicOr(&sh.kids[sh.parent[i]][i >> 5], 1u << (i & 31));
