@@ -21,7 +21,10 @@
 // node's last child, whose residual the draw sums anyway), and the bonus
 // draw one pass that sums the residual over at most 64 consecutive token
 // ranges ("rounds"), then a second over the one round that holds its
-// target.
+// target.  The acceptance tests' inputs depend on the tree alone, so the walk
+// loads them all, a thread per node, before it starts; the same holds for
+// each node's first test (p_res is still p_u), which those threads also
+// take, so a run of accepted first children costs one LDS read per node.
 #include <limits.h>
 
 #include "device_common.h"
@@ -57,12 +60,14 @@ struct Shared {
   int32_t path[kMaxSampledNodes];
   int32_t out[kMaxSampledNodes];
   uint32_t kids[kMaxSampledNodes][kMaxSampledNodes / 32];  // bit c: node c is a child
-  // for each child c of the node being tested: the two logits of c's token
-  // at the node, c's acceptance uniform and c's own softmax statistics
+  // for each node c: the two logits of c's token at its parent, c's
+  // acceptance uniform and c's own softmax statistics (the root: only its
+  // statistics)
   float kid_p[kMaxSampledNodes];
   float kid_q[kMaxSampledNodes];
   float kid_u[kMaxSampledNodes];
   float4 kid_st[kMaxSampledNodes];
+  int32_t fwd[kMaxSampledNodes];  // node's first child when it passes its test, else -1
   float red_a[kWaves];
   float red_b[kWaves];
   float scan[kThreads];
@@ -499,13 +504,52 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
     for (int i = t; i < n * (kMaxSampledNodes / 32); i += kThreads) words[i] = 0u;
   }
   __syncthreads();
-  for (int i = t + 1; i < n; i += kThreads)  // parent[i] in [0, i): checked above
-    atomicOr(&sh.kids[sh.parent[i]][i >> 5], 1u << (i & 31));
+  // Every node's test inputs depend on the tree alone, not on the path the
+  // walk takes, so one round of loads (a thread per node) fetches them all
+  // before it starts; the walk then reads global memory only in its passes.
+  for (int i = t; i < n; i += kThreads) {
+    if (i > 0) {
+      atomicOr(&sh.kids[sh.parent[i]][i >> 5], 1u << (i & 31));  // parent[i] in [0, i): checked above
+      const int tk = sh.token[i];
+      const int64_t prow_off = (int64_t)(base + sh.parent[i]) * a.row_stride;
+      sh.kid_p[i] = load_one<BF16>((const char *)a.target_logits + prow_off * ESZ, tk);
+      sh.kid_q[i] = load_one<BF16>((const char *)a.draft_logits + prow_off * ESZ, tk);
+      sh.kid_u[i] = a.u_accept[base + i];
+    }
+    sh.kid_st[i] = a.stats[base + i];
+  }
+  __syncthreads();
+  // A node's first child is tested against the target distribution itself
+  // (nothing rejected yet), so that test too depends on the tree alone:
+  // thread u takes it for node u, with the arithmetic of the walk's own
+  // test below, and the walk then follows passing first children with one
+  // read per node.
+  for (int i = t; i < n; i += kThreads) {
+    int c = -1;
+#pragma unroll
+    for (int w = kMaxSampledNodes / 32 - 1; w >= 0; --w)
+      if (sh.kids[i][w]) c = 32 * w + __builtin_ctz(sh.kids[i][w]);
+    if (c >= 0) {
+      const float4 st = sh.kid_st[i];
+      const float ip = 1.f / st.y, iq = 1.f / st.w;
+      const float pt = exp2f((sh.kid_p[c] - st.x) * kLog2e) * ip;
+      const float qt = exp2f((sh.kid_q[c] - st.z) * kLog2e) * iq;
+      if (!(sh.kid_u[c] * qt < pt)) c = -1;
+    }
+    sh.fwd[i] = c;
+  }
   __syncthreads();
 
   int u = 0, len = 1;  // current node, path length
   if (t == 0) sh.path[0] = 0;
   while (true) {
+    for (int v; (v = __builtin_amdgcn_readfirstlane(sh.fwd[u])) >= 0; u = v) {
+      if (t == 0) {
+        sh.out[len - 1] = sh.token[v];
+        sh.path[len] = v;
+      }
+      ++len;
+    }
     const char *prow = (const char *)a.target_logits + ((int64_t)(base + u) * a.row_stride) * ESZ;
     const char *qrow = (const char *)a.draft_logits + ((int64_t)(base + u) * a.row_stride) * ESZ;
     uint32_t kids[kMaxSampledNodes / 32];
@@ -526,18 +570,7 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
 #pragma unroll
     for (int w = 0; w < kMaxSampledNodes / 32; ++w)
       if (kids[w]) last_child = 32 * w + 31 - __builtin_clz(kids[w]);
-    // One round of loads for every child's test inputs (thread c takes
-    // child c); the tests themselves run in order below.  The accepted
-    // child's statistics are then already here when it becomes the node.
-    if (t < n && ((sh.kids[u][t >> 5] >> (t & 31)) & 1u)) {
-      const int tk = sh.token[t];
-      sh.kid_p[t] = load_one<BF16>(prow, tk);
-      sh.kid_q[t] = load_one<BF16>(qrow, tk);
-      sh.kid_u[t] = a.u_accept[base + t];
-      sh.kid_st[t] = a.stats[base + t];
-    }
-    const float4 st = u == 0 ? a.stats[base] : sh.kid_st[u];
-    __syncthreads();
+    const float4 st = sh.kid_st[u];
     Residual R;
     R.mp = st.x;
     R.ip = 1.f / st.y;

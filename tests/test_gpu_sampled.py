@@ -291,3 +291,43 @@ def test_depth_limit_boundary(torch_cuda):
         assert ((alen >= 1) == ok).all() and ((ref[0] >= 1) == ok).all(), (K, alen, ref[0])
         if not ok:
             assert (tok == -1).all() and (nodes == -1).all()
+
+
+def test_passing_first_children_at_every_depth(torch_cuda):
+    """A draft row equal to its target row passes every first child's test
+    (u q(t) < p(t) whenever u < 1), so the walk follows first children down to
+    a leaf: a 128-node chain to the full depth limit, and random trees of up to
+    128 nodes.  The other requests keep a noisy draft, so links that pass sit
+    next to rejections and later children in the same batch."""
+    rng = np.random.Generator(np.random.PCG64(13))
+    V, K = 4096, 128
+    parents = [chain_tree(128), chain_tree(2)] + [random_tree(rng, int(n), d) for n, d in
+                                                  [(128, 40), (128, 127), (90, 8), (64, 3), (128, 20), (33, 32)]]
+    indptr = np.cumsum([0] + [p.size for p in parents]).astype(np.int32)
+    parent = np.concatenate(parents)
+    T = int(indptr[-1])
+    tl = (rng.standard_normal((T, V)) * 2).astype(np.float32)
+    hot = rng.integers(0, V, size=T)
+    tl[np.arange(T), hot] = 9.0
+    dl = make_draft_logits(rng, tl, V, "f32", 1.0)
+    equal = [0, 1, 2, 3, 6]
+    for r in equal:
+        dl[indptr[r]:indptr[r + 1]] = tl[indptr[r]:indptr[r + 1]]
+    draft = np.zeros(T, np.int32)
+    for i in range(T):
+        if parent[i] >= 0:
+            p = int(np.searchsorted(indptr, i, side="right") - 1)
+            pr = indptr[p] + parent[i]
+            draft[i] = hot[pr] if rng.random() < 0.7 else rng.integers(0, V)
+    ua, ub = make_uniforms(rng, T), make_uniforms(rng, T)
+    check(torch_cuda, indptr, parent, draft, tl, dl, V, ua, ub, K, "f32")
+    got = _run(torch_cuda, indptr, parent, draft, tl, dl, V, ua, ub, K)
+    assert got[0][0] == 128 and (got[2][0] == np.arange(128)).all()
+    for r in equal:   # every first child passes: the path is the first-child chain to a leaf
+        base, n = int(indptr[r]), int(indptr[r + 1] - indptr[r])
+        kids = [[c for c in range(1, n) if parent[base + c] == v] for v in range(n)]
+        v, path = 0, [0]
+        while kids[v]:
+            v = kids[v][0]
+            path.append(v)
+        assert got[0][r] == len(path) and list(got[2][r][:len(path)]) == path
