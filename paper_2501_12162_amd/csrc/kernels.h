@@ -162,8 +162,20 @@ struct SampledArgs {
   int32_t *accept_len;          // [B]
   int32_t *accept_tokens;       // [B, max_accept]
   int32_t *accept_nodes;        // [B, max_accept]
-  float4 *stats;                // [total_nodes] workspace: (max_p, sum_p, max_q, sum_q)
+  float4 *stats;                // [total_nodes, stats_split] workspace: (max_p, sum_p, max_q, sum_q)
+  int32_t stats_split;          // workgroups per node in the statistics pass
 };
+
+// Workgroups that share one node's statistics pass, each over a contiguous
+// part of its rows: enough that a small batch still puts several on every
+// compute unit (one per node when the batch alone does).
+constexpr int32_t kMaxSampledStatsSplit = 8;
+inline int32_t sampled_stats_split(int64_t total_nodes) {
+  constexpr int64_t kTargetGroups = 4096;
+  if (total_nodes <= 0 || total_nodes >= kTargetGroups) return 1;
+  const int64_t s = (kTargetGroups + total_nodes - 1) / total_nodes;
+  return (int32_t)(s < kMaxSampledStatsSplit ? s : kMaxSampledStatsSplit);
+}
 
 hipError_t launch_sampled_accept(const SampledArgs &a, bool bf16, hipStream_t stream);
 

@@ -345,8 +345,11 @@ __device__ int residual_draw(const char *prow, const char *qrow, int vocab, cons
   return residual_draw_t<BF16>(prow, qrow, vocab, ResidualPass<false>(R), u, sh);
 }
 
-// Softmax statistics of every node's target and draft rows: one workgroup
-// per node, both rows in one pass.  stats[node] = (max_p, sum_p, max_q, sum_q).
+// Softmax statistics of every node's target and draft rows, both rows in one
+// pass: stats_split workgroups per node, each over a contiguous range of
+// whole vectors (the last also takes the tokens past the last vector);
+// stats[node * stats_split + part] = (max_p, sum_p, max_q, sum_q) of part
+// `part`, merged by the walk.
 // NT: the rows are read with the non-temporal hint, for batches whose rows
 // do not fit the last-level cache anyway (see launch_sampled_accept).
 template <bool BF16, bool NT>
@@ -354,7 +357,7 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
   constexpr int EPV = BF16 ? 8 : 4;
   constexpr int ESZ = BF16 ? 2 : 4;
   __shared__ float red[4][kStatsThreads / 64];
-  const int node = blockIdx.x;
+  const int node = blockIdx.x / a.stats_split, part = blockIdx.x % a.stats_split;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const char *prow = (const char *)a.target_logits + (int64_t)node * a.row_stride * ESZ;
   const char *qrow = (const char *)a.draft_logits + (int64_t)node * a.row_stride * ESZ;
@@ -367,6 +370,8 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
     }
   };
   const int nvec = a.vocab / EPV;
+  const int vb = (int)((int64_t)nvec * part / a.stats_split);
+  const int ve = (int)((int64_t)nvec * (part + 1) / a.stats_split);
   auto load = [&](const char *row, int i) -> u32x4 {
     if constexpr (NT) return __builtin_nontemporal_load((const u32x4 *)(row + (int64_t)i * 16));
     return *(const u32x4 *)(row + (int64_t)i * 16);
@@ -398,8 +403,8 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
   // Four vectors of each row in flight per thread: all eight loads are
   // written before the first use (the branches of `take` end the
   // scheduler's regions, so it cannot hoist later loads above them).
-  int i = t;
-  for (; i + 3 * kStatsThreads < nvec; i += 4 * kStatsThreads) {
+  int i = vb + t;
+  for (; i + 3 * kStatsThreads < ve; i += 4 * kStatsThreads) {
     u32x4 w[4], z[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -409,8 +414,8 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
 #pragma unroll
     for (int k = 0; k < 4; ++k) take(w[k], z[k]);
   }
-  for (; i < nvec; i += kStatsThreads) take(load(prow, i), load(qrow, i));
-  for (int v = nvec * EPV + t; v < a.vocab; v += kStatsThreads) {
+  for (; i < ve; i += kStatsThreads) take(load(prow, i), load(qrow, i));
+  for (int v = nvec * EPV + t; part == a.stats_split - 1 && v < a.vocab; v += kStatsThreads) {
     add(mp, sp, load_one<BF16>(prow, v));
     add(mq, sq, load_one<BF16>(qrow, v));
   }
@@ -442,7 +447,7 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
       if (red[0][w] > -INFINITY) Sp += red[1][w] * exp2f((red[0][w] - Mp) * kLog2e);
       if (red[2][w] > -INFINITY) Sq += red[3][w] * exp2f((red[2][w] - Mq) * kLog2e);
     }
-    a.stats[node] = make_float4(Mp, Sp, Mq, Sq);
+    a.stats[blockIdx.x] = make_float4(Mp, Sp, Mq, Sq);
   }
 }
 
@@ -516,7 +521,29 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
       sh.kid_q[i] = load_one<BF16>((const char *)a.draft_logits + prow_off * ESZ, tk);
       sh.kid_u[i] = a.u_accept[base + i];
     }
-    sh.kid_st[i] = a.stats[base + i];
+    // the parts' (max, sum) pairs merged; one part is taken as it is
+    const float4 *ps = a.stats + (int64_t)(base + i) * a.stats_split;
+    float4 st = ps[0];
+    if (a.stats_split > 1) {
+      float4 pp[kMaxSampledStatsSplit];
+#pragma unroll
+      for (int j = 0; j < kMaxSampledStatsSplit; ++j) pp[j] = ps[min(j, a.stats_split - 1)];
+      float mp = -INFINITY, mq = -INFINITY, sp = 0.f, sq = 0.f;
+#pragma unroll
+      for (int j = 0; j < kMaxSampledStatsSplit; ++j)
+        if (j < a.stats_split) {
+          mp = fmaxf(mp, pp[j].x);
+          mq = fmaxf(mq, pp[j].z);
+        }
+#pragma unroll
+      for (int j = 0; j < kMaxSampledStatsSplit; ++j)
+        if (j < a.stats_split) {
+          if (pp[j].x > -INFINITY) sp += pp[j].y * exp2f((pp[j].x - mp) * kLog2e);
+          if (pp[j].z > -INFINITY) sq += pp[j].w * exp2f((pp[j].z - mq) * kLog2e);
+        }
+      st = make_float4(mp, sp, mq, sq);
+    }
+    sh.kid_st[i] = st;
   }
   __syncthreads();
   // A node's first child is tested against the target distribution itself
@@ -640,7 +667,7 @@ hipError_t launch_sampled_accept(const SampledArgs &a, bool bf16, hipStream_t st
     // the call 6% slower); larger batches stream it (4-8% faster measured).
     const double row_bytes = 2.0 * (double)a.total_nodes * a.vocab * (bf16 ? 2 : 4);
     const bool nt = row_bytes > (double)kLastLevelCacheBytes;
-    const dim3 grid((unsigned)a.total_nodes), block(kStatsThreads);
+    const dim3 grid((unsigned)(a.total_nodes * a.stats_split)), block(kStatsThreads);
     if (bf16) {
       if (nt) hipLaunchKernelGGL((sampled_stats_kernel<true, true>), grid, block, 0, stream, a);
       else hipLaunchKernelGGL((sampled_stats_kernel<true, false>), grid, block, 0, stream, a);

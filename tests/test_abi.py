@@ -333,7 +333,7 @@ def test_beam_empty_batch_is_a_noop(lib):
 def _sampled(lib, **kw):
     args = dict(B=2, T=10, indptr=FAKE, par=FAKE, draft=FAKE, tl=0x1000 * 16, dl=0x2000 * 16, stride=1024, V=1000,
                 dtype=ada.ADASERVE_BF16, ua=FAKE, ub=FAKE, K=8, alen=FAKE, tok=FAKE, nodes=FAKE, ws=0x100000,
-                ws_bytes=160)
+                ws_bytes=lib.adaserve_tree_accept_sampled_workspace_bytes(10))
     args.update(kw)
     return lib.adaserve_tree_accept_sampled(args["B"], args["T"], args["indptr"], args["par"], args["draft"],
                                             args["tl"], args["dl"], args["stride"], args["V"], args["dtype"],
@@ -355,7 +355,7 @@ def _sampled(lib, **kw):
     (dict(ub=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
     (dict(nodes=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
     (dict(ws=None), ada.ADASERVE_ERR_WORKSPACE),
-    (dict(ws_bytes=159), ada.ADASERVE_ERR_WORKSPACE),
+    (dict(ws_bytes=10 * 8 * 16 - 1), ada.ADASERVE_ERR_WORKSPACE),  # 10 nodes: 8 statistics parts each
     (dict(ws=0x100000 + 8), ada.ADASERVE_ERR_INVALID_ARGUMENT),   # workspace not 16-byte aligned
 ])
 def test_sampled_accept_rejects_bad_arguments(lib, kw, code):
@@ -370,5 +370,9 @@ def test_sampled_accept_empty_batch_is_a_noop(lib):
 
 def test_sampled_accept_workspace_query(lib):
     assert lib.adaserve_tree_accept_sampled_workspace_bytes(0) == 0
-    assert lib.adaserve_tree_accept_sampled_workspace_bytes(586) == 586 * 16
+    # 16 bytes per node and statistics part; parts: ceil(4096 / total_nodes), 1 to 8
+    assert lib.adaserve_tree_accept_sampled_workspace_bytes(586) == 586 * 7 * 16
+    assert lib.adaserve_tree_accept_sampled_workspace_bytes(1) == 8 * 16
+    assert lib.adaserve_tree_accept_sampled_workspace_bytes(4096) == 4096 * 16
+    assert lib.adaserve_tree_accept_sampled_workspace_bytes(2052) == 2052 * 2 * 16
     assert lib.adaserve_tree_accept_sampled_workspace_bytes(-1) == SIZE_MAX

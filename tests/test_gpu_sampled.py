@@ -133,7 +133,7 @@ def _batch(rng, B, vocab, dtype, max_nodes, depth, noise, row_pad=0):
 
 @pytest.mark.parametrize("seed,dtype,vocab,noise", [(0, "bf16", 32000, 0.3), (1, "bf16", 1000, 1.5),
                                                     (2, "f32", 5003, 0.5), (3, "bf16", 128256, 0.5),
-                                                    (4, "f32", 17, 1.0)])
+                                                    (4, "f32", 17, 1.0), (7, "bf16", 1, 1.0), (8, "f32", 3, 0.5)])
 def test_random_batches(torch_cuda, seed, dtype, vocab, noise):
     rng = np.random.Generator(np.random.PCG64(500 + seed))
     pad = (-vocab) % (8 if dtype == "bf16" else 4)
@@ -152,6 +152,19 @@ def test_vocabularies_past_64_vector_groups(torch_cuda, seed, dtype, vocab):
     args = _batch(rng, 4, vocab, dtype, 4, 3, 0.5, row_pad=pad)
     exact = check(torch_cuda, *args[:5], vocab, *args[5:], 8, dtype)
     assert exact >= 3
+
+
+@pytest.mark.parametrize("seed,B,parts", [(11, 40, 2), (12, 80, 1)])
+def test_statistics_parts_of_large_batches(torch_cuda, seed, B, parts):
+    """The statistics pass splits each node's rows over ceil(4096 / T)
+    workgroups (at most 8) that the walk merges: these batches take two parts
+    per node and one (no merge); the smaller batches above take 7 or 8."""
+    rng = np.random.Generator(np.random.PCG64(900 + seed))
+    args = _batch(rng, B, 64, "bf16", 128, 12, 0.5)
+    T = int(args[0][-1])
+    assert -(-4096 // T) == parts if parts > 1 else T >= 4096
+    exact = check(torch_cuda, *args[:5], 64, *args[5:], 16, "bf16")
+    assert exact >= B - 3
 
 
 def test_llama3_8b_batch(torch_cuda):
