@@ -397,8 +397,8 @@ int32_t adaserve_beam_step(int32_t num_requests, int32_t beam_in, const void *lo
  * u_accept, u_bonus: [total_nodes] fp32 (device).  Logits 16-byte aligned,
  * row_stride * element size a multiple of 16 bytes.  workspace: at least
  * adaserve_tree_accept_sampled_workspace_bytes(total_nodes) bytes of device
- * memory (every node's softmax statistics, in parts: 16 bytes per node and
- * part, 1 to 8 parts per node, fewer the larger the batch), 16-byte aligned,
+ * memory (1 KB per node: every node's softmax statistics, in parts of 16
+ * bytes, up to 64 per node), 16-byte aligned,
  * no initialisation needed; calls sharing a workspace must not overlap in
  * time.  Two kernels are enqueued on `stream`: the statistics of every node
  * (the whole chip), then the walks, one workgroup per request.

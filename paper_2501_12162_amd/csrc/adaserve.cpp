@@ -492,7 +492,7 @@ size_t adaserve_tree_accept_sampled_workspace_bytes(int32_t total_nodes) {
     fail(ADASERVE_ERR_INVALID_ARGUMENT, "total_nodes %d < 0", total_nodes);
     return SIZE_MAX;
   }
-  return (size_t)total_nodes * sampled_stats_split(total_nodes) * 16;
+  return (size_t)total_nodes * kSampledMaxRounds * 16;  // the most statistics parts a node can take
 }
 
 int32_t adaserve_tree_accept_sampled(int32_t num_requests, int32_t total_nodes, const int32_t *node_indptr,
@@ -520,7 +520,8 @@ int32_t adaserve_tree_accept_sampled(int32_t num_requests, int32_t total_nodes, 
   if (!aligned(target_logits, 16) || !aligned(draft_logits, 16) || (row_stride * esz) % 16 != 0)
     return fail(ADASERVE_ERR_INVALID_ARGUMENT,
                 "logits must be 16-byte aligned with rows a multiple of 16 bytes apart");
-  const size_t need = (size_t)total_nodes * sampled_stats_split(total_nodes) * 16;
+  const SampledStatsParts parts = sampled_stats_parts(total_nodes, vocab, dtype == ADASERVE_BF16);
+  const size_t need = (size_t)total_nodes * parts.parts * 16;
   if (need > 0 && (!workspace || workspace_bytes < need))
     return fail(ADASERVE_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace ? workspace_bytes : (size_t)0,
                 need);
@@ -544,7 +545,8 @@ int32_t adaserve_tree_accept_sampled(int32_t num_requests, int32_t total_nodes, 
   a.accept_tokens = accept_tokens;
   a.accept_nodes = accept_nodes;
   a.stats = (float4 *)workspace;
-  a.stats_split = sampled_stats_split(total_nodes);
+  a.stats_parts = parts.parts;
+  a.stats_sub = parts.sub;
   return launch_status(launch_sampled_accept(a, dtype == ADASERVE_BF16, (hipStream_t)stream), "sampled accept launch");
 }
 

@@ -162,19 +162,45 @@ struct SampledArgs {
   int32_t *accept_len;          // [B]
   int32_t *accept_tokens;       // [B, max_accept]
   int32_t *accept_nodes;        // [B, max_accept]
-  float4 *stats;                // [total_nodes, stats_split] workspace: (max_p, sum_p, max_q, sum_q)
-  int32_t stats_split;          // workgroups per node in the statistics pass
+  float4 *stats;                // [total_nodes, stats_parts] workspace: (max_p, sum_p, max_q, sum_q)
+  int32_t stats_parts;          // statistics parts (workgroups) per node: rounds * stats_sub
+  int32_t stats_sub;            // parts per round
 };
 
-// Workgroups that share one node's statistics pass, each over a contiguous
-// part of its rows: enough that a small batch still puts several on every
-// compute unit (one per node when the batch alone does).
-constexpr int32_t kMaxSampledStatsSplit = 8;
-inline int32_t sampled_stats_split(int64_t total_nodes) {
-  constexpr int64_t kTargetGroups = 4096;
-  if (total_nodes <= 0 || total_nodes >= kTargetGroups) return 1;
-  const int64_t s = (kTargetGroups + total_nodes - 1) / total_nodes;
-  return (int32_t)(s < kMaxSampledStatsSplit ? s : kMaxSampledStatsSplit);
+// Round layout of a sampled-verification pass over a row of `vocab` logits,
+// epv of them per 16-byte vector: the vectors go in groups of
+// kSampledGroupVecs, gpr consecutive groups form a round (a contiguous token
+// range), at most kSampledMaxRounds of them; the tokens past the last whole
+// vector belong to the last round.
+constexpr int kSampledGroupVecs = 4096;
+constexpr int kSampledMaxRounds = 64;
+struct SampledRounds {
+  int nvec, ngroups, gpr, nrounds;
+  __host__ __device__ SampledRounds(int vocab, int epv) {
+    nvec = vocab / epv;
+    ngroups = (nvec + kSampledGroupVecs - 1) / kSampledGroupVecs;
+    if (ngroups < 1) ngroups = 1;
+    gpr = (ngroups + kSampledMaxRounds - 1) / kSampledMaxRounds;
+    nrounds = (ngroups + gpr - 1) / gpr;
+  }
+};
+
+// The statistics pass splits each round of every node's rows into `sub`
+// contiguous parts, one workgroup each: enough parts that a small batch
+// still puts several workgroups on every compute unit (4096 in all, at most
+// 8 per node unless the rounds alone are more), at most kSampledMaxRounds
+// per node.
+struct SampledStatsParts {
+  int32_t parts, sub;
+};
+inline SampledStatsParts sampled_stats_parts(int64_t total_nodes, int32_t vocab, bool bf16) {
+  constexpr int64_t kTargetGroups = 4096, kMaxWanted = 8;
+  int64_t want = total_nodes > 0 ? (kTargetGroups + total_nodes - 1) / total_nodes : 1;
+  if (want > kMaxWanted) want = kMaxWanted;
+  const int32_t nrounds = SampledRounds(vocab, bf16 ? 8 : 4).nrounds;
+  int32_t sub = (int32_t)((want + nrounds - 1) / nrounds);
+  if (sub * nrounds > kSampledMaxRounds) sub = kSampledMaxRounds / nrounds;
+  return {nrounds * sub, sub};
 }
 
 hipError_t launch_sampled_accept(const SampledArgs &a, bool bf16, hipStream_t stream);

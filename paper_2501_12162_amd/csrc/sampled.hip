@@ -39,8 +39,9 @@ constexpr int kStatsThreads = 256;
 constexpr int64_t kLastLevelCacheBytes = 256ll << 20;   // MI355X MALL (Infinity Cache)
 constexpr int kWaves = kThreads / 64;
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kGroupVecs = 4 * kThreads;  // 16-byte vectors per pass iteration (four per thread)
-constexpr int kMaxRounds = 64;            // token ranges whose masses a pass keeps (one per lane)
+constexpr int kGroupVecs = kSampledGroupVecs;  // 16-byte vectors per pass iteration (four per thread)
+constexpr int kMaxRounds = kSampledMaxRounds;  // token ranges whose masses a pass keeps (one per lane)
+static_assert(kGroupVecs == 4 * kThreads, "a group is four vectors per thread");
 
 template <bool BF16>
 __device__ __forceinline__ float elem(const u32x4 &w, int e) {
@@ -125,16 +126,9 @@ __device__ __forceinline__ bool q_enters(const Residual &R) { return R.has_q && 
 // kGroupVecs (in a group, thread t takes vectors t, t + kThreads, t +
 // 2 kThreads and t + 3 kThreads, so the loads coalesce); gpr consecutive
 // groups form a round, a contiguous token range, at most kMaxRounds of them.
-// The tokens past the last whole vector belong to the last round.
-struct Rounds {
-  int nvec, ngroups, gpr, nrounds;
-  __device__ Rounds(int vocab, int epv) {
-    nvec = vocab / epv;
-    ngroups = max(1, (nvec + kGroupVecs - 1) / kGroupVecs);
-    gpr = (ngroups + kMaxRounds - 1) / kMaxRounds;
-    nrounds = (ngroups + gpr - 1) / gpr;
-  }
-};
+// The tokens past the last whole vector belong to the last round.  The
+// statistics pass keeps its parts inside these rounds.
+using Rounds = SampledRounds;
 
 // Sum over the vocabulary of the residual.
 template <bool BF16, class RT>
@@ -235,14 +229,12 @@ __device__ float residual_rounds(const char *prow, const char *qrow, int vocab, 
 // Inverse-CDF draw from the residual: the smallest v whose cumulative mass
 // (in token order) exceeds u * (total mass); the last token of nonzero mass
 // when rounding leaves the target past the end (-1 when no token has mass).
-// One coalesced pass finds the round that holds the target; that round is
-// then read once more, each thread taking a contiguous run of its vectors so
+// With the rounds' masses in sh.cum (inclusive prefix), the round that holds
+// the target is read, each thread taking a contiguous run of its vectors so
 // that per-thread sums scan in token order.
 template <bool BF16, class RT>
-__device__ int residual_draw_t(const char *prow, const char *qrow, int vocab, const RT &R, float u,
-                               Shared &sh) {
+__device__ int draw_in_rounds(const char *prow, const char *qrow, int vocab, const RT &R, float u, Shared &sh) {
   constexpr int EPV = BF16 ? 8 : 4;
-  residual_rounds<BF16>(prow, qrow, vocab, R, sh);
   const Rounds rd(vocab, EPV);
   const int t = threadIdx.x, lane = t & 63;
   const float total = sh.cum[rd.nrounds - 1];
@@ -338,18 +330,52 @@ __device__ int residual_draw_t(const char *prow, const char *qrow, int vocab, co
   return pick;
 }
 
+// The rounds' masses of the target distribution p itself (nothing rejected
+// at the node), from the statistics pass's parts of the node's row: `sub`
+// consecutive parts per round, part j's (max, sum) rescaled to the node's
+// (R.mp, 1 / R.ip); inclusive prefix into sh.cum.  No pass over the row.
+__device__ void target_rounds(const Residual &R, const float4 *parts, int sub, int nrounds, Shared &sh) {
+  const int t = threadIdx.x;
+  if (t < 64) {
+    float m = 0.f;
+    if (t < nrounds * sub) {
+      const float4 e = parts[t];
+      if (e.x > -INFINITY) m = e.y * exp2f((e.x - R.mp) * kLog2e) * R.ip;
+    }
+    float rm = 0.f;  // lane r: round r's mass (nrounds * sub <= 64 lanes)
+    for (int k = 0; k < sub; ++k) rm += __shfl(m, min(t * sub + k, 63), 64);
+    if (t >= nrounds) rm = 0.f;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const float o = __shfl_up(rm, off, 64);
+      if (t >= off) rm += o;
+    }
+    if (t < nrounds) sh.cum[t] = rm;
+  }
+  __syncthreads();
+}
+
+// The bonus draw: from p itself, the rounds' masses come from the statistics
+// parts (one read of one round); with q in the residual, one coalesced pass
+// over both rows sums them first.
 template <bool BF16>
 __device__ int residual_draw(const char *prow, const char *qrow, int vocab, const Residual &R, float u,
-                             Shared &sh) {
-  if (q_enters(R)) return residual_draw_t<BF16>(prow, qrow, vocab, ResidualPass<true>(R), u, sh);
-  return residual_draw_t<BF16>(prow, qrow, vocab, ResidualPass<false>(R), u, sh);
+                             const float4 *parts, int sub, Shared &sh) {
+  if (q_enters(R)) {
+    const ResidualPass<true> P(R);
+    residual_rounds<BF16>(prow, qrow, vocab, P, sh);
+    return draw_in_rounds<BF16>(prow, qrow, vocab, P, u, sh);
+  }
+  target_rounds(R, parts, sub, Rounds(vocab, BF16 ? 8 : 4).nrounds, sh);
+  return draw_in_rounds<BF16>(prow, qrow, vocab, ResidualPass<false>(R), u, sh);
 }
 
 // Softmax statistics of every node's target and draft rows, both rows in one
-// pass: stats_split workgroups per node, each over a contiguous range of
-// whole vectors (the last also takes the tokens past the last vector);
-// stats[node * stats_split + part] = (max_p, sum_p, max_q, sum_q) of part
-// `part`, merged by the walk.
+// pass: stats_parts workgroups per node, stats_sub contiguous pieces of each
+// round (the last also takes the tokens past the last vector);
+// stats[node * stats_parts + part] = (max_p, sum_p, max_q, sum_q) of part
+// `part`.  The walk merges them into the node's statistics, and a bonus draw
+// from p reads its rounds' masses off them.
 // NT: the rows are read with the non-temporal hint, for batches whose rows
 // do not fit the last-level cache anyway (see launch_sampled_accept).
 template <bool BF16, bool NT>
@@ -357,7 +383,7 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
   constexpr int EPV = BF16 ? 8 : 4;
   constexpr int ESZ = BF16 ? 2 : 4;
   __shared__ float red[4][kStatsThreads / 64];
-  const int node = blockIdx.x / a.stats_split, part = blockIdx.x % a.stats_split;
+  const int node = blockIdx.x / a.stats_parts, part = blockIdx.x % a.stats_parts;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const char *prow = (const char *)a.target_logits + (int64_t)node * a.row_stride * ESZ;
   const char *qrow = (const char *)a.draft_logits + (int64_t)node * a.row_stride * ESZ;
@@ -369,9 +395,13 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
       m = nm;
     }
   };
-  const int nvec = a.vocab / EPV;
-  const int vb = (int)((int64_t)nvec * part / a.stats_split);
-  const int ve = (int)((int64_t)nvec * (part + 1) / a.stats_split);
+  const Rounds rd(a.vocab, EPV);
+  const int nvec = rd.nvec;
+  const int round = part / a.stats_sub, piece = part % a.stats_sub;
+  const int64_t r0 = (int64_t)round * rd.gpr * kGroupVecs;
+  const int64_t r1 = min((int64_t)nvec, r0 + (int64_t)rd.gpr * kGroupVecs);
+  const int vb = (int)(r0 + (r1 - r0) * piece / a.stats_sub);
+  const int ve = (int)(r0 + (r1 - r0) * (piece + 1) / a.stats_sub);
   auto load = [&](const char *row, int i) -> u32x4 {
     if constexpr (NT) return __builtin_nontemporal_load((const u32x4 *)(row + (int64_t)i * 16));
     return *(const u32x4 *)(row + (int64_t)i * 16);
@@ -415,7 +445,7 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
     for (int k = 0; k < 4; ++k) take(w[k], z[k]);
   }
   for (; i < ve; i += kStatsThreads) take(load(prow, i), load(qrow, i));
-  for (int v = nvec * EPV + t; part == a.stats_split - 1 && v < a.vocab; v += kStatsThreads) {
+  for (int v = nvec * EPV + t; part == a.stats_parts - 1 && v < a.vocab; v += kStatsThreads) {
     add(mp, sp, load_one<BF16>(prow, v));
     add(mq, sq, load_one<BF16>(qrow, v));
   }
@@ -522,25 +552,34 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
       sh.kid_u[i] = a.u_accept[base + i];
     }
     // the parts' (max, sum) pairs merged; one part is taken as it is
-    const float4 *ps = a.stats + (int64_t)(base + i) * a.stats_split;
+    const int np = a.stats_parts;
+    const float4 *ps = a.stats + (int64_t)(base + i) * np;
     float4 st = ps[0];
-    if (a.stats_split > 1) {
-      float4 pp[kMaxSampledStatsSplit];
-#pragma unroll
-      for (int j = 0; j < kMaxSampledStatsSplit; ++j) pp[j] = ps[min(j, a.stats_split - 1)];
+    if (np > 1) {
+      // eight parts' loads at a time, merged into running (max, sum) pairs
       float mp = -INFINITY, mq = -INFINITY, sp = 0.f, sq = 0.f;
+      for (int j0 = 0; j0 < np; j0 += 8) {
+        float4 pp[8];
 #pragma unroll
-      for (int j = 0; j < kMaxSampledStatsSplit; ++j)
-        if (j < a.stats_split) {
-          mp = fmaxf(mp, pp[j].x);
-          mq = fmaxf(mq, pp[j].z);
-        }
+        for (int k = 0; k < 8; ++k) pp[k] = ps[min(j0 + k, np - 1)];
+        float cp = mp, cq = mq;
 #pragma unroll
-      for (int j = 0; j < kMaxSampledStatsSplit; ++j)
-        if (j < a.stats_split) {
-          if (pp[j].x > -INFINITY) sp += pp[j].y * exp2f((pp[j].x - mp) * kLog2e);
-          if (pp[j].z > -INFINITY) sq += pp[j].w * exp2f((pp[j].z - mq) * kLog2e);
-        }
+        for (int k = 0; k < 8; ++k)
+          if (j0 + k < np) {
+            cp = fmaxf(cp, pp[k].x);
+            cq = fmaxf(cq, pp[k].z);
+          }
+        sp = mp > -INFINITY ? sp * exp2f((mp - cp) * kLog2e) : 0.f;
+        sq = mq > -INFINITY ? sq * exp2f((mq - cq) * kLog2e) : 0.f;
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          if (j0 + k < np) {
+            if (pp[k].x > -INFINITY) sp += pp[k].y * exp2f((pp[k].x - cp) * kLog2e);
+            if (pp[k].z > -INFINITY) sq += pp[k].w * exp2f((pp[k].z - cq) * kLog2e);
+          }
+        mp = cp;
+        mq = cq;
+      }
       st = make_float4(mp, sp, mq, sq);
     }
     sh.kid_st[i] = st;
@@ -637,7 +676,8 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
       // so the draw's code is not inlined twice)
       int v = -1;
       for (int attempt = after_last ? 0 : 1; attempt < 2 && v < 0; ++attempt)
-        v = residual_draw<BF16>(prow, qrow, a.vocab, attempt == 0 ? R2 : R, a.u_bonus[base + u], sh);
+        v = residual_draw<BF16>(prow, qrow, a.vocab, attempt == 0 ? R2 : R, a.u_bonus[base + u],
+                                a.stats + (int64_t)(base + u) * a.stats_parts, a.stats_sub, sh);
       if (t == 0) sh.out[len - 1] = v;
       break;
     }
@@ -667,7 +707,7 @@ hipError_t launch_sampled_accept(const SampledArgs &a, bool bf16, hipStream_t st
     // the call 6% slower); larger batches stream it (4-8% faster measured).
     const double row_bytes = 2.0 * (double)a.total_nodes * a.vocab * (bf16 ? 2 : 4);
     const bool nt = row_bytes > (double)kLastLevelCacheBytes;
-    const dim3 grid((unsigned)(a.total_nodes * a.stats_split)), block(kStatsThreads);
+    const dim3 grid((unsigned)(a.total_nodes * a.stats_parts)), block(kStatsThreads);
     if (bf16) {
       if (nt) hipLaunchKernelGGL((sampled_stats_kernel<true, true>), grid, block, 0, stream, a);
       else hipLaunchKernelGGL((sampled_stats_kernel<true, false>), grid, block, 0, stream, a);

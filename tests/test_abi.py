@@ -355,7 +355,7 @@ def _sampled(lib, **kw):
     (dict(ub=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
     (dict(nodes=None), ada.ADASERVE_ERR_INVALID_ARGUMENT),
     (dict(ws=None), ada.ADASERVE_ERR_WORKSPACE),
-    (dict(ws_bytes=10 * 8 * 16 - 1), ada.ADASERVE_ERR_WORKSPACE),  # 10 nodes: 8 statistics parts each
+    (dict(ws_bytes=10 * 8 * 16 - 1), ada.ADASERVE_ERR_WORKSPACE),  # 10 nodes, vocab 1000: 8 parts each
     (dict(ws=0x100000 + 8), ada.ADASERVE_ERR_INVALID_ARGUMENT),   # workspace not 16-byte aligned
 ])
 def test_sampled_accept_rejects_bad_arguments(lib, kw, code):
@@ -370,9 +370,8 @@ def test_sampled_accept_empty_batch_is_a_noop(lib):
 
 def test_sampled_accept_workspace_query(lib):
     assert lib.adaserve_tree_accept_sampled_workspace_bytes(0) == 0
-    # 16 bytes per node and statistics part; parts: ceil(4096 / total_nodes), 1 to 8
-    assert lib.adaserve_tree_accept_sampled_workspace_bytes(586) == 586 * 7 * 16
-    assert lib.adaserve_tree_accept_sampled_workspace_bytes(1) == 8 * 16
-    assert lib.adaserve_tree_accept_sampled_workspace_bytes(4096) == 4096 * 16
-    assert lib.adaserve_tree_accept_sampled_workspace_bytes(2052) == 2052 * 2 * 16
+    # 16 bytes per node and statistics part, sized for the most parts a node
+    # can take (64: one per token range of a draw's pass)
+    assert lib.adaserve_tree_accept_sampled_workspace_bytes(586) == 586 * 64 * 16
+    assert lib.adaserve_tree_accept_sampled_workspace_bytes(1) == 64 * 16
     assert lib.adaserve_tree_accept_sampled_workspace_bytes(-1) == SIZE_MAX

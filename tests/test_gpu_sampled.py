@@ -142,11 +142,14 @@ def test_random_batches(torch_cuda, seed, dtype, vocab, noise):
     assert exact >= 10
 
 
-@pytest.mark.parametrize("seed,dtype,vocab", [(5, "f32", 1_100_003), (6, "bf16", 2_200_007)])
+@pytest.mark.parametrize("seed,dtype,vocab", [(5, "f32", 1_100_003), (6, "bf16", 2_200_007),
+                                              (7, "bf16", 2_097_151)])
 def test_vocabularies_past_64_vector_groups(torch_cuda, seed, dtype, vocab):
     """Vocabularies whose rows hold more than 64 groups of 4096 vectors, so a
     bonus draw's token ranges span two groups each and the last one ends in a
-    partial group and a few tokens past the last whole vector."""
+    partial group and a few tokens past the last whole vector; and one of
+    exactly 64 groups (the most token ranges, and statistics parts, a node
+    takes)."""
     rng = np.random.Generator(np.random.PCG64(500 + seed))
     pad = (-vocab) % (8 if dtype == "bf16" else 4)
     args = _batch(rng, 4, vocab, dtype, 4, 3, 0.5, row_pad=pad)
@@ -156,9 +159,11 @@ def test_vocabularies_past_64_vector_groups(torch_cuda, seed, dtype, vocab):
 
 @pytest.mark.parametrize("seed,B,parts", [(11, 40, 2), (12, 80, 1)])
 def test_statistics_parts_of_large_batches(torch_cuda, seed, B, parts):
-    """The statistics pass splits each node's rows over ceil(4096 / T)
-    workgroups (at most 8) that the walk merges: these batches take two parts
-    per node and one (no merge); the smaller batches above take 7 or 8."""
+    """The statistics pass splits each token range of a node's rows (one
+    range at this vocabulary) into ceil(4096 / T) parts (at most 8), which the
+    walk merges and a draw from p reads: these batches take two parts per
+    node and one (no merge); the smaller batches above take 8, and at vocab
+    128256 two parts in each of four ranges."""
     rng = np.random.Generator(np.random.PCG64(900 + seed))
     args = _batch(rng, B, 64, "bf16", 128, 12, 0.5)
     T = int(args[0][-1])
