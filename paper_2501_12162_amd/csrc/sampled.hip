@@ -71,7 +71,7 @@ struct Shared {
   int32_t fwd[kMaxSampledNodes];  // node's first child when it passes its test, else -1
   float red_a[kWaves];
   float red_b[kWaves];
-  float scan[kThreads];
+  float scan[kWaves];  // the draw's per-wave sums
   float rsum[kMaxRounds][kWaves];  // per round and wave: the residual's mass
   float cum[kMaxRounds];           // inclusive prefix of the rounds' masses, in token order
   int32_t bad;
@@ -257,18 +257,24 @@ __device__ int draw_in_rounds(const char *prow, const char *qrow, int vocab, con
   const int64_t tv0 = min(ve, vb + (int64_t)t * cv), tv1 = min(ve, tv0 + cv);
   const bool tail = rs == rd.nrounds - 1 && t == kThreads - 1;  // tokens past the last vector
   // one pass over this thread's tokens, in order: their mass, the last one
-  // with mass, and (find) the first at which start + running mass > goal
-  auto run = [&](float start, float goal, bool stop, int &found, int &last) {
+  // with mass, and (find) the first at which start + running mass > goal.
+  // The vectors go through w / z four at a time; when the run is one such
+  // chunk (always for rounds of one group) of the target row alone, a second
+  // pass reuses them (both rows' would not fit the registers).
+  u32x4 w[4], z[4];
+  const bool one_chunk = !RT::kQ && tv1 - tv0 <= 4;
+  auto run = [&](float start, float goal, bool stop, bool reuse, int &found, int &last) {
     float acc = start;
     found = -1;
     last = -1;
     for (int64_t i = tv0; i < tv1; i += 4) {
-      u32x4 w[4], z[4];
+      if (!reuse) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int64_t j = min(i + k, tv1 - 1);
-        w[k] = *(const u32x4 *)(prow + j * 16);
-        z[k] = RT::kQ ? *(const u32x4 *)(qrow + j * 16) : w[k];
+        for (int k = 0; k < 4; ++k) {
+          const int64_t j = min(i + k, tv1 - 1);
+          w[k] = *(const u32x4 *)(prow + j * 16);
+          z[k] = RT::kQ ? *(const u32x4 *)(qrow + j * 16) : w[k];
+        }
       }
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
@@ -296,22 +302,29 @@ __device__ int draw_in_rounds(const char *prow, const char *qrow, int vocab, con
     return acc - start;
   };
   int found, last;
-  const float s = run(0.f, 0.f, false, found, last);
-  // inclusive prefix of the threads' sums within the round
-  sh.scan[t] = s;
+  const float s = run(0.f, 0.f, false, false, found, last);
+  // inclusive prefix of the threads' sums within the round: by shuffles
+  // within each wave, then each wave's offset as the sequential sum of the
+  // earlier waves' totals, so that every thread's start is bit for bit the
+  // previous thread's end (exactly one thread holds the target)
+  float x = s;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float o = __shfl_up(x, off, 64);
+    if (lane >= off) x += o;
+  }
+  const int wave = t >> 6;
+  if (lane == 63) sh.scan[wave] = x;
   if (t == 0) sh.pick = -1;
   __syncthreads();
-  for (int off = 1; off < kThreads; off <<= 1) {
-    const float add = t >= off ? sh.scan[t - off] : 0.f;
-    __syncthreads();
-    sh.scan[t] += add;
-    __syncthreads();
-  }
-  const float lo = before + (t > 0 ? sh.scan[t - 1] : 0.f);  // exactly the previous thread's end
-  const float hi = before + sh.scan[t];
+  float woff = 0.f;
+  for (int k = 0; k < wave; ++k) woff += sh.scan[k];
+  const float xprev = __shfl_up(x, 1, 64);
+  const float lo = before + (lane > 0 ? woff + xprev : woff);
+  const float hi = before + (woff + x);
   if (find && s > 0.f && lo <= target && target < hi) {
     int f, l2;
-    run(lo, target, true, f, l2);
+    run(lo, target, true, one_chunk, f, l2);
     sh.pick = f >= 0 ? min(f, last) : last;
   }
   __syncthreads();
