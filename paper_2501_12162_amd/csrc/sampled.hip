@@ -508,65 +508,26 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
   const int32_t n = a.node_indptr[r + 1] - base;
   const bool shape_ok = n >= 1 && n <= kMaxSampledNodes && base >= 0 && base + n <= a.total_nodes;
   if (t == 0) sh.bad = shape_ok ? 0 : 1;
-  __syncthreads();
   if (shape_ok) {
-    for (int i = t; i < n; i += kThreads) {
-      const int32_t p = a.parent[base + i];
-      const int32_t tk = a.draft_tokens[base + i];
-      sh.parent[i] = p;
-      sh.token[i] = tk;
-      const bool ok = i == 0 ? p == -1 : (p >= 0 && p < i && tk >= 0 && tk < a.vocab);
-      if (!ok) atomicOr(&sh.bad, 1);
-    }
-  }
-  __syncthreads();
-  if (!sh.bad) {
-    // every node's depth must be below the output rows (K): each thread
-    // follows its nodes' parent chains, at most K steps (parents come first,
-    // checked above, so every chain reaches the root)
-    bool deep = false;
-    for (int i = t; i < n; i += kThreads) {
-      int v = i, d = 0;
-      while (v != 0 && d < K) {
-        v = sh.parent[v];
-        ++d;
-      }
-      deep |= d >= K;
-    }
-    if (deep) atomicOr(&sh.bad, 1);
-  }
-  __syncthreads();
-  if (sh.bad) {
-    for (int k = t; k < K; k += kThreads) {
-      otok[k] = -1;
-      onode[k] = -1;
-    }
-    if (t == 0) *alen = -1;
-    return;
-  }
-
-  // every node's children as a bit set, built once for the walk (which
-  // takes a node's children in index order: lowest set bit first)
-  {
+    // every node's children as a bit set, built below for the walk (which
+    // takes a node's children in index order: lowest set bit first)
     uint32_t *words = &sh.kids[0][0];
     for (int i = t; i < n * (kMaxSampledNodes / 32); i += kThreads) words[i] = 0u;
   }
   __syncthreads();
-  // Every node's test inputs depend on the tree alone, not on the path the
-  // walk takes, so one round of loads (a thread per node) fetches them all
-  // before it starts; the walk then reads global memory only in its passes.
-  for (int i = t; i < n; i += kThreads) {
-    if (i > 0) {
-      atomicOr(&sh.kids[sh.parent[i]][i >> 5], 1u << (i & 31));  // parent[i] in [0, i): checked above
-      const int tk = sh.token[i];
-      const int64_t prow_off = (int64_t)(base + sh.parent[i]) * a.row_stride;
-      sh.kid_p[i] = load_one<BF16>((const char *)a.target_logits + prow_off * ESZ, tk);
-      sh.kid_q[i] = load_one<BF16>((const char *)a.draft_logits + prow_off * ESZ, tk);
-      sh.kid_u[i] = a.u_accept[base + i];
-    }
+  // A thread per node (n <= kMaxSampledNodes < kThreads): its parent and
+  // token, checked; its uniform and statistics in the same round of loads;
+  // then, for a well-formed node, its token's two logits at its parent.
+  // Every test input depends on the tree alone, not on the path the walk
+  // takes, so the walk reads global memory only in its passes.
+  static_assert(kMaxSampledNodes <= kThreads, "a thread per node");
+  if (shape_ok && t < n) {
+    const int32_t p = a.parent[base + t];
+    const int32_t tk = a.draft_tokens[base + t];
+    const float ua = t > 0 ? a.u_accept[base + t] : 0.f;
     // the parts' (max, sum) pairs merged; one part is taken as it is
     const int np = a.stats_parts;
-    const float4 *ps = a.stats + (int64_t)(base + i) * np;
+    const float4 *ps = a.stats + (int64_t)(base + t) * np;
     float4 st = ps[0];
     if (np > 1) {
       // eight parts' loads at a time, merged into running (max, sum) pairs
@@ -595,15 +556,50 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
       }
       st = make_float4(mp, sp, mq, sq);
     }
-    sh.kid_st[i] = st;
+    sh.parent[t] = p;
+    sh.token[t] = tk;
+    sh.kid_st[t] = st;
+    sh.kid_u[t] = ua;
+    const bool ok = t == 0 ? p == -1 : (p >= 0 && p < t && tk >= 0 && tk < a.vocab);
+    if (!ok) {
+      atomicOr(&sh.bad, 1);
+    } else if (t > 0) {
+      atomicOr(&sh.kids[p][t >> 5], 1u << (t & 31));
+      const int64_t prow_off = (int64_t)(base + p) * a.row_stride;
+      sh.kid_p[t] = load_one<BF16>((const char *)a.target_logits + prow_off * ESZ, tk);
+      sh.kid_q[t] = load_one<BF16>((const char *)a.draft_logits + prow_off * ESZ, tk);
+    }
   }
   __syncthreads();
+  if (!sh.bad) {
+    // every node's depth must be below the output rows (K): each thread
+    // follows its node's parent chain, at most K steps (parents come first,
+    // checked above, so every chain reaches the root)
+    if (t < n) {
+      int v = t, d = 0;
+      while (v != 0 && d < K) {
+        v = sh.parent[v];
+        ++d;
+      }
+      if (d >= K) atomicOr(&sh.bad, 1);
+    }
+  }
+  __syncthreads();
+  if (sh.bad) {
+    for (int k = t; k < K; k += kThreads) {
+      otok[k] = -1;
+      onode[k] = -1;
+    }
+    if (t == 0) *alen = -1;
+    return;
+  }
   // A node's first child is tested against the target distribution itself
   // (nothing rejected yet), so that test too depends on the tree alone:
   // thread u takes it for node u, with the arithmetic of the walk's own
   // test below, and the walk then follows passing first children with one
   // read per node.
-  for (int i = t; i < n; i += kThreads) {
+  if (t < n) {
+    const int i = t;
     int c = -1;
 #pragma unroll
     for (int w = kMaxSampledNodes / 32 - 1; w >= 0; --w)
