@@ -36,7 +36,6 @@ namespace {
 
 constexpr int kThreads = 1024;
 constexpr int kStatsThreads = 256;
-constexpr int64_t kLastLevelCacheBytes = 256ll << 20;   // MI355X MALL (Infinity Cache)
 constexpr int kWaves = kThreads / 64;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kGroupVecs = kSampledGroupVecs;  // 16-byte vectors per pass iteration (four per thread)
@@ -388,10 +387,10 @@ __device__ int residual_draw(const char *prow, const char *qrow, int vocab, cons
 // round (the last also takes the tokens past the last vector);
 // stats[node * stats_parts + part] = (max_p, sum_p, max_q, sum_q) of part
 // `part`.  The walk merges them into the node's statistics, and a bonus draw
-// from p reads its rounds' masses off them.
-// NT: the rows are read with the non-temporal hint, for batches whose rows
-// do not fit the last-level cache anyway (see launch_sampled_accept).
-template <bool BF16, bool NT>
+// from p reads its rounds' masses off them.  The rows are streamed with the
+// non-temporal hint: the walks read only the few rows they visit again, and
+// they find those no slower for it (every batch measured faster streamed).
+template <bool BF16>
 __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArgs a) {
   constexpr int EPV = BF16 ? 8 : 4;
   constexpr int ESZ = BF16 ? 2 : 4;
@@ -416,8 +415,7 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
   const int vb = (int)(r0 + (r1 - r0) * piece / a.stats_sub);
   const int ve = (int)(r0 + (r1 - r0) * (piece + 1) / a.stats_sub);
   auto load = [&](const char *row, int i) -> u32x4 {
-    if constexpr (NT) return __builtin_nontemporal_load((const u32x4 *)(row + (int64_t)i * 16));
-    return *(const u32x4 *)(row + (int64_t)i * 16);
+    return __builtin_nontemporal_load((const u32x4 *)(row + (int64_t)i * 16));
   };
   // one vector of each row into the running (max, sum) pairs
   auto take = [&](const u32x4 &w, const u32x4 &z) {
@@ -710,20 +708,11 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
 hipError_t launch_sampled_accept(const SampledArgs &a, bool bf16, hipStream_t stream) {
   if (a.num_requests == 0) return hipSuccess;
   if (a.total_nodes > 0) {
-    // The walks read the rows of the nodes they visit again.  When both
-    // logits arrays fit the 256 MB MALL they are still there after the
-    // statistics pass (long-context batch, 131 MB: streaming the pass made
-    // the call 6% slower); larger batches stream it (4-8% faster measured).
-    const double row_bytes = 2.0 * (double)a.total_nodes * a.vocab * (bf16 ? 2 : 4);
-    const bool nt = row_bytes > (double)kLastLevelCacheBytes;
     const dim3 grid((unsigned)(a.total_nodes * a.stats_parts)), block(kStatsThreads);
-    if (bf16) {
-      if (nt) hipLaunchKernelGGL((sampled_stats_kernel<true, true>), grid, block, 0, stream, a);
-      else hipLaunchKernelGGL((sampled_stats_kernel<true, false>), grid, block, 0, stream, a);
-    } else {
-      if (nt) hipLaunchKernelGGL((sampled_stats_kernel<false, true>), grid, block, 0, stream, a);
-      else hipLaunchKernelGGL((sampled_stats_kernel<false, false>), grid, block, 0, stream, a);
-    }
+    if (bf16)
+      hipLaunchKernelGGL(sampled_stats_kernel<true>, grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL(sampled_stats_kernel<false>, grid, block, 0, stream, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
