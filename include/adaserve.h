@@ -375,8 +375,8 @@ int32_t adaserve_beam_step(int32_t num_requests, int32_t beam_in, const void *lo
  * Row u of target_logits / draft_logits ([total_nodes, row_stride], dtype)
  * holds the target / draft model's logits after node u's root path, already
  * divided by the sampling temperature; p_u / q_u are their softmax over
- * columns 0 .. vocab - 1.  Draft rows of leaves are read (by the statistics
- * pass) but never affect the result.  From the
+ * columns 0 .. vocab - 1.  Draft rows of leaves are not read (q at a leaf
+ * enters no test and no residual).  From the
  * root, the children of the current node u are tried in index order: child
  * c with token t = draft_tokens[c] is accepted when
  *   u_accept[c] * q_u(t) < p_res(t)
@@ -393,7 +393,10 @@ int32_t adaserve_beam_step(int32_t num_requests, int32_t beam_in, const void *lo
  * accept_nodes[r] = the path from the root, accept_tokens[r] = the accepted
  * drafts' tokens then the bonus token, -1 past them; accept_len = -1 and rows
  * of -1 for a malformed tree (as adaserve_tree_accept), a draft token of a
- * non-root node outside [0, vocab), or a tree deeper than max_accept - 1.
+ * non-root node outside [0, vocab), a tree deeper than max_accept - 1, or a
+ * node with children whose draft row has no finite logit.  node_indptr must
+ * be increasing (requests of consecutive, disjoint node ranges): where it is
+ * not, requests that share nodes may also get -1.
  * u_accept, u_bonus: [total_nodes] fp32 (device).  Logits 16-byte aligned,
  * row_stride * element size a multiple of 16 bytes.  workspace: at least
  * adaserve_tree_accept_sampled_workspace_bytes(total_nodes) bytes of device

@@ -27,6 +27,8 @@
 // take, so a run of accepted first children costs one LDS read per node.
 #include <limits.h>
 
+#include <type_traits>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -382,11 +384,36 @@ __device__ int residual_draw(const char *prow, const char *qrow, int vocab, cons
   return draw_in_rounds<BF16>(prow, qrow, vocab, ResidualPass<false>(R), u, sh);
 }
 
+// Whether node g may have a child, so that its draft row is needed (q_g
+// enters only the tests of g's children and the residuals at g).  The
+// request that holds g is found by a 64-ary search of node_indptr (ballots
+// over one wave's loads), then its later nodes are checked for g's local id
+// as their parent.  Whatever does not fit a well-formed batch (node_indptr
+// not increasing, a request longer than kMaxSampledNodes) answers true, so
+// the row is read.  Wave-uniform.
+__device__ bool node_may_have_children(const SampledArgs &a, int g) {
+  const int lane = threadIdx.x & 63;
+  int lo = 0, hi = a.num_requests;  // the request is in [lo, hi)
+  while (hi - lo > 1) {
+    const int step = (hi - lo + 63) / 64;
+    const int k = lo + lane * step;
+    const uint64_t m = __ballot(k < hi && a.node_indptr[k] <= g);
+    if (!m) return true;
+    lo += (63 - __clzll((unsigned long long)m)) * step;
+    hi = min(hi, lo + step);
+  }
+  const int base = a.node_indptr[lo], end = a.node_indptr[lo + 1];
+  if (!(base <= g && g < end && end - base <= kMaxSampledNodes && end <= a.total_nodes)) return true;
+  bool kid = false;
+  for (int j = g + 1 + lane; j < end; j += 64) kid |= a.parent[j] == g - base;
+  return __ballot(kid) != 0;
+}
+
 // Softmax statistics of every node's target and draft rows, both rows in one
 // pass: stats_parts workgroups per node, stats_sub contiguous pieces of each
 // round (the last also takes the tokens past the last vector);
 // stats[node * stats_parts + part] = (max_p, sum_p, max_q, sum_q) of part
-// `part`.  The walk merges them into the node's statistics, and a bonus draw
+// `part`; a leaf's draft row is not read (max_q = -inf, sum_q = 0).  The walk merges them into the node's statistics, and a bonus draw
 // from p reads its rounds' masses off them.  The rows are streamed with the
 // non-temporal hint: the walks read only the few rows they visit again, and
 // they find those no slower for it (every batch measured faster streamed).
@@ -417,49 +444,54 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
   auto load = [&](const char *row, int i) -> u32x4 {
     return __builtin_nontemporal_load((const u32x4 *)(row + (int64_t)i * 16));
   };
-  // one vector of each row into the running (max, sum) pairs
-  auto take = [&](const u32x4 &w, const u32x4 &z) {
-    float wm = elem<BF16>(w, 0), zm = elem<BF16>(z, 0);
+  // one vector of a row into its running (max, sum) pair
+  auto take = [&](const u32x4 &w, float &m, float &s) {
+    float wm = elem<BF16>(w, 0);
 #pragma unroll
-    for (int e = 1; e < EPV; ++e) {
-      wm = fmaxf(wm, elem<BF16>(w, e));
-      zm = fmaxf(zm, elem<BF16>(z, e));
-    }
-    const float nmp = fmaxf(mp, wm), nmq = fmaxf(mq, zm);
-    if (nmp > -INFINITY) {
+    for (int e = 1; e < EPV; ++e) wm = fmaxf(wm, elem<BF16>(w, e));
+    const float nm = fmaxf(m, wm);
+    if (nm > -INFINITY) {
       float acc = 0.f;
 #pragma unroll
-      for (int e = 0; e < EPV; ++e) acc += __builtin_amdgcn_exp2f((elem<BF16>(w, e) - nmp) * kLog2e);
-      sp = (mp > -INFINITY ? sp * __builtin_amdgcn_exp2f((mp - nmp) * kLog2e) : 0.f) + acc;
-      mp = nmp;
-    }
-    if (nmq > -INFINITY) {
-      float acc = 0.f;
-#pragma unroll
-      for (int e = 0; e < EPV; ++e) acc += __builtin_amdgcn_exp2f((elem<BF16>(z, e) - nmq) * kLog2e);
-      sq = (mq > -INFINITY ? sq * __builtin_amdgcn_exp2f((mq - nmq) * kLog2e) : 0.f) + acc;
-      mq = nmq;
+      for (int e = 0; e < EPV; ++e) acc += __builtin_amdgcn_exp2f((elem<BF16>(w, e) - nm) * kLog2e);
+      s = (m > -INFINITY ? s * __builtin_amdgcn_exp2f((m - nm) * kLog2e) : 0.f) + acc;
+      m = nm;
     }
   };
-  // Four vectors of each row in flight per thread: all eight loads are
-  // written before the first use (the branches of `take` end the
-  // scheduler's regions, so it cannot hoist later loads above them).
-  int i = vb + t;
-  for (; i + 3 * kStatsThreads < ve; i += 4 * kStatsThreads) {
-    u32x4 w[4], z[4];
+  // The pass over the target row, and the draft row when Q: four vectors of
+  // each row in flight per thread, all loads written before the first use
+  // (the branches of `take` end the scheduler's regions, so it cannot hoist
+  // later loads above them; and with the draft row's loads under a runtime
+  // test, the compiler would wait for them all at its join).
+  auto pass = [&](auto with_q) {
+    constexpr bool Q = decltype(with_q)::value;
+    int i = vb + t;
+    for (; i + 3 * kStatsThreads < ve; i += 4 * kStatsThreads) {
+      u32x4 w[4], z[4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      w[k] = load(prow, i + k * kStatsThreads);
-      z[k] = load(qrow, i + k * kStatsThreads);
+      for (int k = 0; k < 4; ++k) {
+        w[k] = load(prow, i + k * kStatsThreads);
+        if constexpr (Q) z[k] = load(qrow, i + k * kStatsThreads);
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        take(w[k], mp, sp);
+        if constexpr (Q) take(z[k], mq, sq);
+      }
     }
-#pragma unroll
-    for (int k = 0; k < 4; ++k) take(w[k], z[k]);
-  }
-  for (; i < ve; i += kStatsThreads) take(load(prow, i), load(qrow, i));
-  for (int v = nvec * EPV + t; part == a.stats_parts - 1 && v < a.vocab; v += kStatsThreads) {
-    add(mp, sp, load_one<BF16>(prow, v));
-    add(mq, sq, load_one<BF16>(qrow, v));
-  }
+    for (; i < ve; i += kStatsThreads) {
+      take(load(prow, i), mp, sp);
+      if constexpr (Q) take(load(qrow, i), mq, sq);
+    }
+    for (int v = nvec * EPV + t; part == a.stats_parts - 1 && v < a.vocab; v += kStatsThreads) {
+      add(mp, sp, load_one<BF16>(prow, v));
+      if constexpr (Q) add(mq, sq, load_one<BF16>(qrow, v));
+    }
+  };
+  if (node_may_have_children(a, node))
+    pass(std::true_type{});
+  else
+    pass(std::false_type{});
   // (max, sum) pairs over the workgroup
   float wmp = mp, wmq = mq;
 #pragma unroll
@@ -572,14 +604,19 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
   if (!sh.bad) {
     // every node's depth must be below the output rows (K): each thread
     // follows its node's parent chain, at most K steps (parents come first,
-    // checked above, so every chain reaches the root)
+    // checked above, so every chain reaches the root).  A node with children
+    // needs its draft statistics: max_q = -inf means that its draft row has
+    // no finite logit (q undefined), or that the statistics pass took it for
+    // a leaf (a node_indptr that is not increasing); either way the request
+    // is not verified.
     if (t < n) {
       int v = t, d = 0;
       while (v != 0 && d < K) {
         v = sh.parent[v];
         ++d;
       }
-      if (d >= K) atomicOr(&sh.bad, 1);
+      const bool has_kids = (sh.kids[t][0] | sh.kids[t][1] | sh.kids[t][2] | sh.kids[t][3]) != 0u;
+      if (d >= K || (has_kids && !(sh.kid_st[t].z > -INFINITY))) atomicOr(&sh.bad, 1);
     }
   }
   __syncthreads();

@@ -349,3 +349,59 @@ def test_passing_first_children_at_every_depth(torch_cuda):
             v = kids[v][0]
             path.append(v)
         assert got[0][r] == len(path) and list(got[2][r][:len(path)]) == path
+
+
+def test_draft_rows_of_leaves_are_not_read(torch_cuda):
+    """The statistics pass skips every leaf's draft row (q at a leaf enters no
+    test and no residual): leaves' draft rows of NaN leave every output bit
+    unchanged.  An internal node whose draft row has no finite logit (q
+    undefined) fails its request alone."""
+    rng = np.random.Generator(np.random.PCG64(31))
+    V, K = 1000, 8
+    indptr, parent, draft, tl, dl, ua, ub = _batch(rng, 10, V, "f32", 40, 6, 0.5)
+    check(torch_cuda, indptr, parent, draft, tl, dl, V, ua, ub, K, "f32")
+    ref = _run(torch_cuda, indptr, parent, draft, tl, dl, V, ua, ub, K)
+    internal = np.zeros(len(parent), bool)
+    for r in range(len(indptr) - 1):
+        for i in range(indptr[r] + 1, indptr[r + 1]):
+            internal[indptr[r] + parent[i]] = True
+    assert (~internal).sum() > 10
+    dl_nan = dl.copy()
+    dl_nan[~internal] = np.nan
+    got = _run(torch_cuda, indptr, parent, draft, tl, dl_nan, V, ua, ub, K)
+    for a, b in zip(ref, got):
+        np.testing.assert_array_equal(a, b)
+    r = next(r for r in range(len(indptr) - 1) if indptr[r + 1] - indptr[r] > 1)
+    dl_inf = dl.copy()
+    dl_inf[indptr[r]] = -np.inf   # the root of request r has children
+    got = _run(torch_cuda, indptr, parent, draft, tl, dl_inf, V, ua, ub, K)
+    assert got[0][r] == -1 and (got[1][r] == -1).all() and (got[2][r] == -1).all()
+    others = np.arange(len(indptr) - 1) != r
+    for a, b in zip(ref, got):
+        np.testing.assert_array_equal(a[others], b[others])
+
+
+def test_overlapping_requests(torch_cuda):
+    """A node_indptr that is not increasing (request 1 has a negative node
+    count, so requests 0 and 2 share nodes 0-2): request 1 fails, and each of
+    the others either fails or matches the oracle on its own nodes -- the
+    statistics pass may take a shared node for a leaf of one of them."""
+    rng = np.random.Generator(np.random.PCG64(32))
+    V, K = 512, 6
+    parent = np.array([-1, 0, 0, 1, 2], np.int32)
+    draft = np.array([0, 5, 9, 7, 3], np.int32)
+    tl = (rng.standard_normal((5, V)) * 2).astype(np.float32)
+    tl[np.arange(5), [5, 7, 3, 1, 2]] = 8.0
+    dl = make_draft_logits(rng, tl, V, "f32", 0.3)
+    ua, ub = make_uniforms(rng, 5), make_uniforms(rng, 5)
+    indptr = np.array([0, 5, 0, 3], np.int32)
+    got = _run(torch_cuda, indptr, parent, draft, tl, dl, V, ua, ub, K)
+    assert got[0][1] == -1
+    for r, (lo, hi) in ((0, (0, 5)), (2, (0, 3))):
+        if got[0][r] == -1:
+            continue
+        alone = _run(torch_cuda, np.array([0, hi - lo], np.int32), parent[lo:hi], draft[lo:hi], tl[lo:hi],
+                     dl[lo:hi], V, ua[lo:hi], ub[lo:hi], K)
+        assert got[0][r] == alone[0][0]
+        np.testing.assert_array_equal(got[1][r], alone[1][0])
+        np.testing.assert_array_equal(got[2][r], alone[2][0])
