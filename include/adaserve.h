@@ -394,7 +394,8 @@ int32_t adaserve_beam_step(int32_t num_requests, int32_t beam_in, const void *lo
  * drafts' tokens then the bonus token, -1 past them; accept_len = -1 and rows
  * of -1 for a malformed tree (as adaserve_tree_accept), a draft token of a
  * non-root node outside [0, vocab), a tree deeper than max_accept - 1, or a
- * node with children whose draft row has no finite logit.  node_indptr must
+ * node with children whose draft row has no logit above -inf (NaN counts as
+ * none: q is then no distribution).  node_indptr must
  * be increasing (requests of consecutive, disjoint node ranges): where it is
  * not, requests that share nodes may also get -1.
  * u_accept, u_bonus: [total_nodes] fp32 (device).  Logits 16-byte aligned,

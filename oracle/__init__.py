@@ -406,8 +406,9 @@ def tree_accept_sampled(*, node_indptr, parent, draft_tokens, target_logits, dra
     Outputs follow tree_accept: accept_len = accepted drafts + 1, accept_nodes
     = the path from the root, accept_tokens = the accepted drafts' tokens then
     the bonus token; -1 for a malformed tree (as tree_accept), a draft token
-    of a non-root node outside [0, vocab), or a tree deeper than
-    max_accept - 1.  For callers comparing against float32 arithmetic, also
+    of a non-root node outside [0, vocab), a tree deeper than
+    max_accept - 1, or a node with children whose draft row has no logit
+    above -inf (q is then no distribution; NaN counts as none).  For callers comparing against float32 arithmetic, also
     returns per request the smallest relative margin of its acceptance tests
     (inf when it took none) and the cumulative distribution the bonus token
     was drawn from (None for a malformed request).  float64 throughout.
@@ -444,6 +445,9 @@ def tree_accept_sampled(*, node_indptr, parent, draft_tokens, target_logits, dra
         for i in range(1, n):
             depth[i] = depth[par[i]] + 1
         if depth.max() > max_accept - 1 or any(not (0 <= draft[base + i] < vocab) for i in range(1, n)):
+            continue
+        if any(not np.any(np.asarray(draft_logits[base + j][:vocab], dtype=np.float64) > -np.inf)
+               for j in set(int(x) for x in par[1:])):
             continue
         u, path, out, m = 0, [0], [], np.inf
         while True:

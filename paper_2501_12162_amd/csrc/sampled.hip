@@ -606,9 +606,9 @@ __global__ __launch_bounds__(kThreads) void sampled_accept_kernel(SampledArgs a)
     // follows its node's parent chain, at most K steps (parents come first,
     // checked above, so every chain reaches the root).  A node with children
     // needs its draft statistics: max_q = -inf means that its draft row has
-    // no finite logit (q undefined), or that the statistics pass took it for
-    // a leaf (a node_indptr that is not increasing); either way the request
-    // is not verified.
+    // no logit above -inf (q is no distribution), or that the statistics
+    // pass took it for a leaf (a node_indptr that is not increasing); either
+    // way the request is not verified.
     if (t < n) {
       int v = t, d = 0;
       while (v != 0 && d < K) {

@@ -379,6 +379,7 @@ def test_draft_rows_of_leaves_are_not_read(torch_cuda):
     others = np.arange(len(indptr) - 1) != r
     for a, b in zip(ref, got):
         np.testing.assert_array_equal(a[others], b[others])
+    check(torch_cuda, indptr, parent, draft, tl, dl_inf, V, ua, ub, K, "f32")   # the oracle fails it too
 
 
 def test_overlapping_requests(torch_cuda):

@@ -162,3 +162,25 @@ def test_malformed_out_of_range_and_too_deep():
     ok = oracle.tree_accept_sampled(node_indptr=[0, 3], parent=[-1, 0, 1], draft_tokens=[9, 1, 2],
                                     max_accept=3, **kw)   # the root's token is never read
     assert ok[0][0] >= 1
+
+
+def test_draft_row_without_mass_at_a_node_with_children():
+    """q must be a distribution where it is used: a node with children whose
+    draft row has no logit above -inf (NaN counts as none) fails the request;
+    the same row at a leaf is never read."""
+    V = 4
+    tl = np.zeros((3, V))
+    kw = dict(node_indptr=[0, 3], parent=[-1, 0, 1], draft_tokens=[0, 1, 2], target_logits=tl, vocab=V,
+              u_accept=[0.5] * 3, u_bonus=[0.5] * 3, max_accept=4)
+    for bad in (-np.inf, np.nan):
+        dl = np.zeros((3, V))
+        dl[1] = bad                    # node 1 has a child (node 2)
+        res = oracle.tree_accept_sampled(draft_logits=dl, **kw)
+        assert res[0][0] == -1 and (res[1] == -1).all() and (res[2] == -1).all()
+        dl = np.zeros((3, V))
+        dl[2] = bad                    # node 2 is a leaf
+        with np.errstate(invalid="ignore"):
+            res = oracle.tree_accept_sampled(draft_logits=dl, **kw)
+        ref = oracle.tree_accept_sampled(draft_logits=np.zeros((3, V)), **kw)
+        for a, b in zip(res[:3], ref[:3]):
+            np.testing.assert_array_equal(a, b)
