@@ -32,17 +32,17 @@ int32_t check_device() {
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(ADASERVE_ERR_DEVICE, "hipGetDevice failed: %s", hipGetErrorString(e));
   static std::mutex mu;
-  static signed char verdict[256];  // 0 unknown, 1 gfx950, -1 other
+  static signed char arch_ok[256];  // 0 unknown, 1 gfx950, -1 other
   if (dev < 0 || dev >= 256) return fail(ADASERVE_ERR_DEVICE, "device ordinal %d out of range", dev);
   std::lock_guard<std::mutex> lock(mu);
-  if (verdict[dev] == 0) {
+  if (arch_ok[dev] == 0) {
     hipDeviceProp_t prop;
     e = hipGetDeviceProperties(&prop, dev);
     if (e != hipSuccess)
       return fail(ADASERVE_ERR_DEVICE, "hipGetDeviceProperties failed: %s", hipGetErrorString(e));
-    verdict[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
+    arch_ok[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
   }
-  if (verdict[dev] < 0) return fail(ADASERVE_ERR_UNSUPPORTED, "device %d is not gfx950", dev);
+  if (arch_ok[dev] < 0) return fail(ADASERVE_ERR_UNSUPPORTED, "device %d is not gfx950", dev);
   return ADASERVE_OK;
 }
 

@@ -1,6 +1,6 @@
 """Summaries of rocprofv3 output for the committed profiles.
 
-Usage (on the GPU machine, after the runs named in each summary's header):
+Usage (on an MI355X, after the runs named in each summary's header):
 
   python -m paper_2501_12162_amd.profiling stats  <kernel_stats.csv> <out.md> "<command>" [<kernel_trace.csv> <warmup> <steps>]
   python -m paper_2501_12162_amd.profiling traffic <fetch_dir> <write_dir> <workload> <out.json> "<commands>"
