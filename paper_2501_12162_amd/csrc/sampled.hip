@@ -463,25 +463,29 @@ __global__ __launch_bounds__(kStatsThreads) void sampled_stats_kernel(SampledArg
   // (the branches of `take` end the scheduler's regions, so it cannot hoist
   // later loads above them; and with the draft row's loads under a runtime
   // test, the compiler would wait for them all at its join).
+  // A part is a few vectors per thread (about 8 of each row at 128256
+  // logits and 8 parts), so its last, partial batch is taken the same way:
+  // slots past the part load its last vector again and are taken as -inf
+  // vectors, which leave every sum bit unchanged (each row is still taken in
+  // the same order).
+  constexpr uint32_t kNegInf = BF16 ? 0xff80ff80u : 0xff800000u;
+  const u32x4 neg_inf = {kNegInf, kNegInf, kNegInf, kNegInf};
   auto pass = [&](auto with_q) {
     constexpr bool Q = decltype(with_q)::value;
-    int i = vb + t;
-    for (; i + 3 * kStatsThreads < ve; i += 4 * kStatsThreads) {
+    for (int i = vb + t; i < ve; i += 4 * kStatsThreads) {
       u32x4 w[4], z[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        w[k] = load(prow, i + k * kStatsThreads);
-        if constexpr (Q) z[k] = load(qrow, i + k * kStatsThreads);
+        const int j = min(i + k * kStatsThreads, ve - 1);
+        w[k] = load(prow, j);
+        if constexpr (Q) z[k] = load(qrow, j);
       }
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        take(w[k], mp, sp);
-        if constexpr (Q) take(z[k], mq, sq);
+        const bool in = i + k * kStatsThreads < ve;
+        take(in ? w[k] : neg_inf, mp, sp);
+        if constexpr (Q) take(in ? z[k] : neg_inf, mq, sq);
       }
-    }
-    for (; i < ve; i += kStatsThreads) {
-      take(load(prow, i), mp, sp);
-      if constexpr (Q) take(load(qrow, i), mq, sq);
     }
     for (int v = nvec * EPV + t; part == a.stats_parts - 1 && v < a.vocab; v += kStatsThreads) {
       add(mp, sp, load_one<BF16>(prow, v));
