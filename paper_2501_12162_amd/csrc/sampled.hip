@@ -14,14 +14,16 @@
 // rejection c grows by the previous S and S is the new residual's mass
 // (if p_res = r/S with r = max(0, p - c q), then max(0, p_res - q) is
 // proportional to max(0, p - (c + S) q)).  A first kernel computes every
-// node's softmax statistics (max and exp-sum of its target and draft rows)
-// across the whole chip; the walk -- one workgroup of 1024 threads per
-// request -- then reads them, so an acceptance test costs two logits, a
-// rejection one pass over the node's two rows (the new S; none after the
-// node's last child, whose residual the draw sums anyway), and the bonus
-// draw one pass that sums the residual over at most 64 consecutive token
-// ranges ("rounds"), then a second over the one round that holds its
-// target.  The acceptance tests' inputs depend on the tree alone, so the walk
+// node's softmax statistics (max and exp-sum of its target row, and of its
+// draft row when it has children) across the whole chip, in parts that
+// follow the token ranges ("rounds", at most 64) of the draw below; the
+// walk -- one workgroup of 1024 threads per request -- then reads them, so
+// an acceptance test costs two logits, a rejection one pass over the node's
+// two rows (the new S; none after the node's last child, whose residual the
+// draw sums anyway), and the bonus draw the residual's mass in each round
+// (from the statistics parts for p itself, else one pass over both rows),
+// then a pass over the one round that holds its target.  The acceptance
+// tests' inputs depend on the tree alone, so the walk
 // loads them all, a thread per node, before it starts; the same holds for
 // each node's first test (p_res is still p_u), which those threads also
 // take, so a run of accepted first children costs one LDS read per node.
