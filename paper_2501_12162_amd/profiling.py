@@ -4,6 +4,7 @@ Usage (on an MI355X, after the runs named in each summary's header):
 
   python -m paper_2501_12162_amd.profiling stats  <kernel_stats.csv> <out.md> "<command>" [<kernel_trace.csv> <warmup> <steps>]
   python -m paper_2501_12162_amd.profiling traffic <fetch_dir> <write_dir> <workload> <out.json> "<commands>"
+  python -m paper_2501_12162_amd.profiling traffic-sampled <fetch_dir> <write_dir> <workload> <out.json> "<commands>"
   python -m paper_2501_12162_amd.profiling counters <out.json> <workload> "<commands>" <dir> [<dir> ...]
 
 ``traffic`` reads the per-dispatch FETCH_SIZE and WRITE_SIZE counters (KiB) of
@@ -66,6 +67,21 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def sampled_source_hash() -> str:
+    """sha256 over the sources that decide the sampled-verification kernels'
+    traffic: sampled.hip and the argument block and parts sizing it shares
+    with the host."""
+    h = hashlib.sha256()
+    csrc = os.path.join(PKG, "csrc")
+    for name in ("sampled.hip", "device_common.h"):
+        with open(os.path.join(csrc, name)) as f:
+            h.update(name.encode())
+            h.update(_code_only(f.read()).encode())
+    with open(os.path.join(csrc, "kernels.h")) as f:
+        h.update(_code_only(_block(f.read(), "struct SampledArgs", "hipError_t launch_sampled_accept")).encode())
+    return h.hexdigest()[:16]
+
+
 def kernel_kind(name: str) -> str:
     if "tree_attn_combine" in name:
         return "tree_attn_combine"
@@ -79,6 +95,10 @@ def kernel_kind(name: str) -> str:
         return "beam_scan"
     if "beam_merge" in name:
         return "beam_merge"
+    if "sampled_stats" in name:
+        return "sampled_stats"
+    if "sampled_accept" in name:
+        return "sampled_accept"
     return "other"
 
 
@@ -139,14 +159,19 @@ def _calibration_factor(rows, expect_bytes: int) -> float:
     return (expect_bytes / 1024.0) / value
 
 
-def traffic_summary(fetch_dir: str, write_dir: str, workload: int, commands: str) -> dict:
+def traffic_summary(fetch_dir: str, write_dir: str, workload: int, commands: str, sampled: bool = False) -> dict:
+    """Calibrated HBM bytes per dispatch (medians) of the verification
+    kernels, or with `sampled` of the sampled-verification kernels (their
+    own source hash)."""
     fetch = _counter_rows(fetch_dir, "FETCH_SIZE")
     write = _counter_rows(write_dir, "WRITE_SIZE")
     f_factor = _calibration_factor(fetch, CALIB_BYTES)
     w_factor = _calibration_factor(write, CALIB_BYTES)
-    res = {"workload": workload, "kernel_source_sha": kernel_source_hash(),
+    res = {"workload": workload, "kernel_source_sha": sampled_source_hash() if sampled else kernel_source_hash(),
            "fetch_factor": f_factor, "write_factor": w_factor, "commands": commands, "kernels": {}}
-    for kind in ("tree_attn", "tree_attn_combine", "node_argmax", "tree_accept"):
+    kinds = ("sampled_stats", "sampled_accept") if sampled else (
+        "tree_attn", "tree_attn_combine", "node_argmax", "tree_accept")
+    for kind in kinds:
         fv = [float(r["Counter_Value"]) for r in fetch if kernel_kind(r["Kernel_Name"]) == kind]
         wv = [float(r["Counter_Value"]) for r in write if kernel_kind(r["Kernel_Name"]) == kind]
         if not fv:
@@ -228,8 +253,9 @@ def main(argv):
         with open(argv[3], "w") as f:
             f.write(md)
         print(md)
-    elif len(argv) >= 6 and argv[1] == "traffic":
-        res = traffic_summary(argv[2], argv[3], int(argv[4]), argv[6] if len(argv) > 6 else "")
+    elif len(argv) >= 6 and argv[1] in ("traffic", "traffic-sampled"):
+        res = traffic_summary(argv[2], argv[3], int(argv[4]), argv[6] if len(argv) > 6 else "",
+                              sampled=argv[1] == "traffic-sampled")
         with open(argv[5], "w") as f:
             json.dump(res, f, indent=1)
         print(json.dumps(res, indent=1))

@@ -106,3 +106,22 @@ def test_timed_step_summary_picks_the_timed_loop(tmp_path):
     assert res["steps"] == 3
     assert res["tree_attn_us"] == 200.0 and res["tree_attn_combine_us"] == 8.0
     assert res["start_to_start_us"] == (200_000 + 1000 + 8_000 + 1000) / 1e3
+
+
+STATS = "void adaserve::(anonymous namespace)::sampled_stats_kernel<true>(adaserve::SampledArgs)"
+WALK = "void adaserve::(anonymous namespace)::sampled_accept_kernel<true>(adaserve::SampledArgs)"
+
+
+def test_sampled_traffic_has_its_own_kernels_and_hash(tmp_path):
+    """The sampled summary keeps the statistics and walk kernels only, under
+    the hash of the sampled sources (which the attention hash does not
+    cover, and the other way round)."""
+    fetch = [(COPY, "FETCH_SIZE", 128 * 1024.0, 5), (ATTN, "FETCH_SIZE", 100.0, 5),
+             (STATS, "FETCH_SIZE", 40.0, 5), (WALK, "FETCH_SIZE", 4.0, 5), (STATS, "FETCH_SIZE", 60.0, 5)]
+    write = [(COPY, "WRITE_SIZE", 256 * 1024.0, 5), (ATTN, "WRITE_SIZE", 10.0, 5), (STATS, "WRITE_SIZE", 1.0, 5)]
+    _write_counters(tmp_path / "f", fetch)
+    _write_counters(tmp_path / "w", write)
+    res = profiling.traffic_summary(str(tmp_path / "f"), str(tmp_path / "w"), 3, "cmd", sampled=True)
+    assert set(res["kernels"]) == {"sampled_stats", "sampled_accept"}
+    assert res["kernels"]["sampled_stats"]["fetch_bytes"] == 50.0 * 1024 * 2.0
+    assert res["kernel_source_sha"] == profiling.sampled_source_hash() != profiling.kernel_source_hash()
