@@ -594,6 +594,11 @@ def main():
     torch.cuda.synchronize()
     sampled_us = commit_ev[0].elapsed_time(commit_ev[1]) * 1e3 / 10
     sampled_len = s_len.cpu().numpy()
+    # algorithmic bytes of the call: every target row and the draft rows of
+    # the nodes with children (a leaf's draft distribution enters no test)
+    starts = np.repeat(b.node_indptr[:-1], np.diff(b.node_indptr))
+    internal = np.unique((starts + b.parent)[b.parent >= 0]).size
+    sampled_bytes = (b.total_nodes + internal) * b.vocab * (2 if is_bf16_in(b) else 4)
 
     if fused:
         # the step's parts timed alone, call after call on the same inputs
@@ -730,6 +735,8 @@ def main():
             "select_candidates": int(cands.cand_prob.size),
             "sampled_accept_us": sampled_us,
             "sampled_accepted_tokens": int(sampled_len.sum()),
+            "sampled_accept_alg_bytes": int(sampled_bytes),
+            "sampled_accept_hbm_frac": sampled_bytes / (sampled_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
             "beam_step_us": beam_us,
             "beam_step_rows": int(bb.logits.shape[0]),
             "beam_step_hbm_frac": beam_bytes / (beam_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
