@@ -133,8 +133,13 @@ def _batch(rng, B, vocab, dtype, max_nodes, depth, noise, row_pad=0):
 
 @pytest.mark.parametrize("seed,dtype,vocab,noise", [(0, "bf16", 32000, 0.3), (1, "bf16", 1000, 1.5),
                                                     (2, "f32", 5003, 0.5), (3, "bf16", 128256, 0.5),
-                                                    (4, "f32", 17, 1.0), (7, "bf16", 1, 1.0), (8, "f32", 3, 0.5)])
+                                                    (4, "f32", 17, 1.0), (7, "bf16", 1, 1.0), (8, "f32", 3, 0.5),
+                                                    (9, "bf16", 65537, 0.5), (10, "f32", 98305, 0.8)])
 def test_random_batches(torch_cuda, seed, dtype, vocab, noise):
+    """Random trees of up to 40 nodes over vocabularies from 1 token to 128256;
+    65537 (bf16: two token ranges of four statistics parts each, one token
+    past the last vector) and 98305 (f32: six ranges of two parts) split the
+    rows unevenly."""
     rng = np.random.Generator(np.random.PCG64(500 + seed))
     pad = (-vocab) % (8 if dtype == "bf16" else 4)
     args = _batch(rng, 12, vocab, dtype, 40, 6, noise, row_pad=pad)
