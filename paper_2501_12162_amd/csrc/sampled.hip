@@ -27,8 +27,6 @@
 // loads them all, a thread per node, before it starts; the same holds for
 // each node's first test (p_res is still p_u), which those threads also
 // take, so a run of accepted first children costs one LDS read per node.
-#include <limits.h>
-
 #include <type_traits>
 
 #include "device_common.h"
@@ -73,7 +71,6 @@ struct Shared {
   float4 kid_st[kMaxSampledNodes];
   int32_t fwd[kMaxSampledNodes];  // node's first child when it passes its test, else -1
   float red_a[kWaves];
-  float red_b[kWaves];
   float scan[kWaves];  // the draw's per-wave sums
   float rsum[kMaxRounds][kWaves];  // per round and wave: the residual's mass
   float cum[kMaxRounds];           // inclusive prefix of the rounds' masses, in token order
