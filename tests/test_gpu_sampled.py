@@ -411,3 +411,23 @@ def test_overlapping_requests(torch_cuda):
         assert got[0][r] == alone[0][0]
         np.testing.assert_array_equal(got[1][r], alone[1][0])
         np.testing.assert_array_equal(got[2][r], alone[2][0])
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_drawn_batches(torch_cuda, seed):
+    """Drawn shapes: 1-12 requests of 1-64 nodes, depth caps 1-12, output rows
+    from the deepest node's need up to 16, vocabularies 1-40000 in either
+    dtype (so the statistics parts, the first-child links, the leaves'
+    skipped draft rows and both kinds of bonus draw all vary), draft noise
+    0.1-2."""
+    rng = np.random.Generator(np.random.PCG64(4000 + seed))
+    B = int(rng.integers(1, 13))
+    vocab = int(rng.choice([1, 2, 7, 8, 9, 100, 1000, 4097, 32768, 32769, int(rng.integers(1, 40001))]))
+    dtype = "bf16" if rng.random() < 0.5 else "f32"
+    depth = int(rng.integers(1, 13))
+    noise = float(rng.uniform(0.1, 2.0))
+    pad = (-vocab) % (8 if dtype == "bf16" else 4)
+    args = _batch(rng, B, vocab, dtype, 64, depth, noise, row_pad=pad)
+    K = int(rng.integers(depth + 1, 17)) if depth + 1 < 17 else 16
+    exact = check(torch_cuda, *args[:5], vocab, *args[5:], K, dtype)
+    assert exact >= B - 2
