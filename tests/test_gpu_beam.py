@@ -272,3 +272,23 @@ def test_final_selection_both_forms(torch_cuda, w_in, w_out):
     rng = np.random.Generator(np.random.PCG64(w_in * 100 + w_out))
     b = make_beam_batch(rng, 3, w_in, 5000)
     check(torch_cuda, b.logits, b.vocab, b.beam_logprob, w_out, "bf16")
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_drawn_shapes(torch_cuda, seed):
+    """Drawn shapes: 1-20 requests of 1-16 beams, 1-24 children kept,
+    vocabularies of 1-200000 tokens in either dtype with padded rows (at most
+    8M logits a batch), logit spreads 0.5-6, root steps and unused beams."""
+    rng = np.random.Generator(np.random.PCG64(7000 + seed))
+    dtype = "bf16" if rng.random() < 0.5 else "f32"
+    vocab = int(rng.choice([1, 2, 15, 16, 17, 4095, 4096, 65536, 65537, int(rng.integers(1, 200001))]))
+    B = int(rng.integers(1, 21))
+    w_in = int(rng.integers(1, 17))
+    while B * w_in * vocab > 8_000_000 and B * w_in > 1:
+        B, w_in = max(1, B // 2), max(1, w_in // 2)
+    w_out = int(rng.integers(1, 25))
+    pad = (-vocab) % (8 if dtype == "bf16" else 4) + int(rng.integers(0, 2)) * 8
+    dead = int(rng.integers(0, w_in)) if rng.random() < 0.3 else 0
+    b = make_beam_batch(rng, B, w_in, vocab, dtype=dtype, std=float(rng.uniform(0.5, 6.0)), row_pad=pad,
+                        root_step=rng.random() < 0.2, dead_beams=dead)
+    check(torch_cuda, b.logits, b.vocab, b.beam_logprob, w_out, dtype)
