@@ -87,3 +87,33 @@ def test_commit_edge_cases_f32_and_in_place(torch_cuda):
     alen = np.array([8, 3, -1, 3, 5, 9, 0], np.int32)   # request 5: len > max_accept
     new_len = _check(torch_cuda, b, alen, nodes, in_place=True)
     assert new_len.tolist() == [16, 32, 5, 0, 10, 2, 16]   # request 3 has no page at all
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_commit_drawn_batches(torch_cuda, seed):
+    """Drawn shapes: 1-10 requests with random trees of 1-40 nodes, prefixes
+    of 0-300 tokens, head layouts and head dims, either dtype, and 0-40
+    tokens of pages reserved past each prefix (too few leave the commit
+    short of pages), acceptance from the oracle."""
+    rng = np.random.Generator(np.random.PCG64(9000 + seed))
+    B = int(rng.integers(1, 11))
+    parents = [random_tree(rng, int(rng.integers(1, 41)), int(rng.integers(1, 12))) for _ in range(B)]
+    hq, hkv = [(4, 1), (8, 2), (32, 8), (16, 16)][int(rng.integers(0, 4))]
+    dtype = "bf16" if rng.random() < 0.5 else "f32"
+    b = make_batch(parents=parents, prefix_lens=rng.integers(0, 301, size=B).tolist(), num_q_heads=hq,
+                   num_kv_heads=hkv, head_dim=int(rng.choice([64, 128])), dtype=dtype, vocab=64,
+                   seed=seed, reserve_tokens=int(rng.choice([0, 3, 8, 40])))
+    alen, _, nodes = oracle.tree_accept(b.node_indptr, b.parent, b.draft_tokens, b.planted_argmax,
+                                        int(max(12, np.max(alen_bound(parents)))))
+    _check(torch_cuda, b, alen, nodes)
+
+
+def alen_bound(parents):
+    """Rows an accepted path can take: the deepest node's depth + 1."""
+    out = []
+    for p in parents:
+        d = np.zeros(p.size, np.int64)
+        for i in range(1, p.size):
+            d[i] = d[p[i]] + 1
+        out.append(int(d.max()) + 1)
+    return out
