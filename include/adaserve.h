@@ -247,9 +247,10 @@ int32_t adaserve_tree_verify_step(int32_t num_requests, const int32_t *node_indp
 /*
  * Accepted-path KV commit: the keys and values of the accepted path enter
  * the request's paged cache, so the next iteration's prefix holds them
- * (section 5.1: the verified tokens are stored back into the request pool for
- * the next iteration; section 2: the root is the last generated token, whose
- * K/V, like every tree node's, was computed in the verification pass).
+ * (section 5.1: once verified, a request's tokens return with it to the pool
+ * of requests that the next iteration draws from; section 2: the root is the
+ * last generated token, whose K/V, like every tree node's, was computed in
+ * the verification pass).
  *
  * For request r with len = accept_len[r] >= 1 and L = prefix_len[r], row
  * k = 0 .. len-1 copies the tree row of local node accept_nodes[r][k]

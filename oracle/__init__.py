@@ -6,7 +6,7 @@ written from the paper's definitions (section 2 draft token trees;
 section 3 Theorem 1 path acceptance; section 4.3 step 4 verification;
 section 5.1 logits returned per node; Appendix B parents before children),
 plus the accepted-path KV commit (``commit_kv``, plain numpy: section 5.1,
-verified tokens stored back for the next iteration), the two selection
+a request's verified tokens carried into its next iteration), the two selection
 phases of Algorithm 2 (``select_trees``, section 4.3 steps 2-3) and one
 beam-search speculation step (``beam_step``, section 4.3 step 1).
 
@@ -168,8 +168,9 @@ def tree_accept_bruteforce(node_indptr, parent, draft_tokens, target_argmax, max
 
 def commit_kv(*, node_indptr, accept_len, accept_nodes, k_tree, v_tree, k_pages, v_pages,
               block_table, prefix_len, page_size: int):
-    """Accepted-path KV commit (section 5.1: the verified tokens are stored back
-    into the request pool for the next iteration; section 2: the root is the
+    """Accepted-path KV commit (section 5.1: once verified, a request's tokens
+    return with it to the pool of requests that the next iteration draws
+    from; section 2: the root is the
     last generated token, so the accepted path root..i* is what the next
     iteration's prefix must hold).
 

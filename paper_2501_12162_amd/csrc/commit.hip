@@ -1,8 +1,8 @@
 // Accepted-path KV commit on gfx950: after acceptance, the keys and values of
 // the accepted root..i* path move from the tree rows into the request's
 // paged cache at positions L_r .. L_r + d*, so that the next iteration sees
-// them as prefix (section 5.1: verified tokens are stored back into the
-// request pool for the next iteration).
+// them as prefix (section 5.1: once verified, a request's tokens return with
+// it to the pool of requests that the next iteration draws from).
 //
 // One workgroup per request, three rounds of dependent loads: the request's
 // scalars; every path row's node and page at once (kept in LDS; the first
